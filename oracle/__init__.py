@@ -1,0 +1,16 @@
+"""CPU oracle of FadeMem's per-chunk cache step (test infrastructure only).
+
+Only tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The product library never does.
+"""
+from .fademem_oracle import (  # noqa: F401
+    Entry,
+    OracleCache,
+    TIE_RTOL,
+    attend,
+    bf16_bits,
+    bf16_from_bits,
+    chunk_step,
+    round_to_bf16,
+    round_to_f32,
+)
