@@ -1,0 +1,166 @@
+/*
+ * fademem.h -- C ABI of the FadeMem per-chunk cache step on one MI355X
+ * (gfx950).  FadeMem: "Distance-Aware Memory Consolidation for
+ * Autoregressive Video Diffusion", arXiv 2606.10671.
+ *
+ * The library keeps, per transformer layer, the bounded ordered memory of
+ * Sec. 3.1 / Sec. 3.3 (at most M entries, each one representative KV block
+ * plus its span s and temporal position mu), updates it with Algorithm S1
+ * (append, power-law distance schedule, adjacent-pair consolidation,
+ * first-frame anchor), and runs the attention of a chunk's queries over
+ * [memory entries in order || current chunk] (Sec. 3.1, Sec. 4.1).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are token-major and contiguous: a block, a query chunk, a
+ *   current chunk and an output are [tokens][heads][head_dim], one batch.
+ *   Element type is fp32 or bf16 as configured (dtype); LSE is fp32.
+ * - Device pointers must be 16-byte aligned; the pool 256-byte aligned.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Every call except fademem_get_state, fademem_entry_kv and
+ *   fademem_merge_log is asynchronous on that stream and never waits for
+ *   the device.  One cache is used by one host thread and one stream at a
+ *   time.
+ * - Ownership: the caller allocates and owns the device pool and every
+ *   Q/K/V/O/LSE buffer.  The library allocates no device memory, never
+ *   frees caller memory and keeps only the pool pointer.  insert copies K
+ *   and V, so the caller may reuse its buffers once the stream has passed
+ *   the call.
+ * - Errors: 0 (FADEMEM_OK) or a negative FADEMEM_E* code.  Arguments and
+ *   state are validated before anything is enqueued, so a call that fails
+ *   validation leaves the cache unchanged.  FADEMEM_EHIP reports a HIP
+ *   launch or runtime failure (see fademem_last_hip_error).  No C++
+ *   exception crosses this interface.
+ */
+#ifndef FADEMEM_H
+#define FADEMEM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  FADEMEM_OK = 0,
+  FADEMEM_EINVAL = -1,     /* bad configuration, argument, pointer or size      */
+  FADEMEM_ESTATE = -2,     /* call not allowed in the current memory state       */
+  FADEMEM_ENOMEM = -3,     /* caller's pool smaller than fademem_pool_bytes      */
+  FADEMEM_EHIP = -4,       /* HIP runtime or launch error                        */
+  FADEMEM_EUNSUPPORTED = -5/* valid request this build does not implement        */
+};
+
+enum { FADEMEM_F32 = 0, FADEMEM_BF16 = 1 };
+
+/* Consolidation operators (Sec. 3.3 "Consolidation operator"; Table 4).
+ * Only the paper's default is implemented in this build. */
+enum { FADEMEM_MERGE_SQRT_SPAN = 0 };
+
+typedef struct fademem_config {
+  int64_t budget;           /* M, the entry budget (Sec. 3.1); 2 <= M <= 1023.
+                               M >= 2 keeps one pair eligible once the newest
+                               entry is protected (Sec. 3.3).                  */
+  int32_t heads;            /* H >= 1                                          */
+  int32_t head_dim;         /* D, 64 or 128                                    */
+  int64_t tokens_per_block; /* N >= 1, tokens of one generation unit (one
+                               latent frame, supplementary Sec. S4)            */
+  double beta;              /* exponent of u(d) = d^beta, 0 < beta <= 1
+                               (Sec. 3.3); the paper's default is 0.3 (Sec. 4.1) */
+  int32_t anchor;           /* 1: the first inserted block is a global anchor
+                               (Sec. 3.3, Alg. S1), the paper's default; 0: off */
+  int32_t merge_op;         /* FADEMEM_MERGE_SQRT_SPAN                          */
+  int32_t dtype;            /* FADEMEM_F32 or FADEMEM_BF16 for K, V, Q, O      */
+  int32_t layers;           /* L >= 1 per-layer memories sharing one schedule.
+                               The schedule depends only on positions, so every
+                               layer makes the same decisions (Sec. 3.3).       */
+} fademem_config;
+
+typedef struct fademem_cache fademem_cache; /* opaque host object */
+
+/* Bytes of device pool a configuration needs: (M+1) KV slots per layer for
+ * K and V, plus the memory's metadata.  Returns EINVAL for a bad config. */
+int fademem_pool_bytes(const fademem_config* cfg, size_t* bytes);
+
+/* Create a cache over a caller-owned device pool of `pool_bytes` bytes
+ * (>= fademem_pool_bytes).  Enqueues the initialisation of the metadata on
+ * `stream` (the pool's previous contents do not matter).  The memory starts
+ * empty.  *out receives a host handle to destroy with fademem_cache_destroy.
+ * Errors: EINVAL (config, NULL or misaligned pool), ENOMEM (pool too small),
+ * EUNSUPPORTED (merge_op), EHIP. */
+int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_bytes,
+                         void* stream, fademem_cache** out);
+
+/* Release the host handle.  The pool stays the caller's.  NULL is a no-op. */
+int fademem_cache_destroy(fademem_cache* cache);
+
+/* Append the block B_t = (K_t, V_t) at position t as the entry (K_t, V_t,
+ * t, 1) -- first step of Alg. S1, Sec. 3.3 "Memory entries and insertion".
+ * k[l], v[l] (host arrays of `layers` device pointers) are layer l's block,
+ * [N][H][D].  Positions are integers that strictly increase (0-indexed by
+ * convention; the first block inserted into an empty memory becomes the
+ * anchor when the option is on), |t| < 2^40.
+ * Errors: EINVAL (NULL/misaligned pointers, position out of range),
+ * ESTATE (position not increasing, or M+1 entries already held: call
+ * fademem_consolidate first), EHIP. */
+int fademem_insert(fademem_cache* cache, const void* const* k, const void* const* v,
+                   int64_t position, void* stream);
+
+/* Rest of Alg. S1.  If the memory holds at most M entries this is a no-op
+ * (and enqueues nothing).  Otherwise, on the device: d_i = t - mu_i with t
+ * the newest position, u = d^beta, gaps |u(d_{i+1}) - u(d_i)| over the
+ * adjacent pairs except the one holding the newest entry, j = the smallest
+ * gap (gaps within a relative 1e-9 of the smallest count as tied and the
+ * oldest such pair wins); the pair is replaced by its consolidation: spans
+ * add, mu is span-weighted; K, V = sqrt-span weighted average evaluated in
+ * fp64 and rounded once (round-to-nearest-even) to the storage type; when
+ * the pair holds the anchor its K, V and position are kept (Sec. 3.3,
+ * Alg. S1).  The decision never crosses to the host.  Errors: EHIP. */
+int fademem_consolidate(fademem_cache* cache, void* stream);
+
+/* Attention of the chunk's queries over layer `layer`'s exposed cache:
+ * O_h = softmax(scale * Q_h K_h^T) V_h per head, with the keys/values
+ * [memory entries in memory order || current chunk] (Sec. 3.1, Sec. 4.1),
+ * no mask.  q and out: [q_tokens][H][D]; k_cur, v_cur: [cur_tokens][H][D]
+ * (cur_tokens may be 0 if the memory is not empty).  scale = 0 selects
+ * 1/sqrt(D).  lse, if not NULL, receives [H][q_tokens] fp32 natural-log
+ * sums of exponentials of the scaled scores.  Accumulation is fp32 (bf16
+ * inputs use bf16 MFMA with fp32 accumulation).  q_tokens = 0 is a no-op.
+ * Errors: EINVAL (layer out of range, NULL/misaligned pointers, no keys at
+ * all, sizes out of range), EHIP. */
+int fademem_attend(fademem_cache* cache, int32_t layer, const void* q, int64_t q_tokens,
+                   const void* k_cur, const void* v_cur, int64_t cur_tokens, float scale,
+                   void* out, float* lse, void* stream);
+
+/* Number of entries currently held (host mirror; never waits). */
+int fademem_count(const fademem_cache* cache, int64_t* count);
+
+/* Copy the memory's metadata to host arrays of at least M+1 elements (any
+ * of them may be NULL): first covered position, span s_i, pos_sum_i (the
+ * integer with mu_i = pos_sum_i / s_i) and the newest position.
+ * Synchronises `stream`.  Errors: EINVAL, EHIP. */
+int fademem_get_state(fademem_cache* cache, int64_t* count, int64_t* first, int64_t* span,
+                      int64_t* pos_sum, int64_t* newest, void* stream);
+
+/* Device pointers of layer `layer`'s logical entry i (0 = oldest), valid
+ * until the next insert/consolidate.  Synchronises `stream`. */
+int fademem_entry_kv(fademem_cache* cache, int32_t layer, int64_t i, const void** k,
+                     const void** v, void* stream);
+
+/* Selected pair indices j of the consolidations run so far, oldest first.
+ * *total receives how many have run; the most recent min(total, cap, 4096)
+ * are copied into j[].  Synchronises `stream`. */
+int fademem_merge_log(fademem_cache* cache, int32_t* j, int64_t cap, int64_t* total,
+                      void* stream);
+
+/* hipError_t value of the last FADEMEM_EHIP on this cache (0 if none). */
+int fademem_last_hip_error(const fademem_cache* cache);
+
+/* Static description of an error code. */
+const char* fademem_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FADEMEM_H */

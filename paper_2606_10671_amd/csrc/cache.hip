@@ -1,0 +1,578 @@
+// FadeMem bounded memory on the device: pool layout, the C ABI, and the
+// bookkeeping kernels (insert copy, schedule, merge).
+//
+// Paper: FadeMem, arXiv 2606.10671 -- Sec. 3.1 (bounded ordered memory),
+// Sec. 3.3 (insertion, distance-aware scheduling, consolidation operator,
+// boundary handling) and Algorithm S1 (the complete update).
+#include <math.h>
+#include <string.h>
+
+#include <new>
+
+#include "fademem_internal.h"
+
+using namespace fademem;
+
+struct fademem_cache {
+  fademem_config cfg;
+  Layout lay;
+  char* pool;
+  int64_t count;        // entries held (mirrors the device state exactly)
+  int64_t newest;       // newest inserted position
+  bool any_inserted;
+  int last_hip_error;
+};
+
+namespace {
+
+inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int hip_fail(fademem_cache* c, hipError_t e) {
+  if (c) c->last_hip_error = int(e);
+  return FADEMEM_EHIP;
+}
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// Kernels
+// ---------------------------------------------------------------------------
+
+// Empty memory: order = identity permutation, counters cleared.
+__global__ void init_kernel(DevHeader* hdr, int32_t* order, int64_t slots) {
+  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    hdr->merges_total = 0;
+    hdr->desc_kind = kMergeNone;
+    hdr->desc_dst_slot = 0;
+    hdr->desc_src_slot = 0;
+    hdr->pad0 = 0;
+    hdr->desc_w_dst = 0.0;
+    hdr->desc_w_src = 0.0;
+  }
+  if (i < slots) order[i] = int32_t(i);
+}
+
+struct InsertArgs {
+  const void* k[kMaxLayersPerLaunch];
+  const void* v[kMaxLayersPerLaunch];
+  char* pool;
+  Layout lay;
+  int64_t layer0;      // first layer of this launch
+  int64_t units;       // 16-byte units per block
+  int64_t index;       // logical index of the new entry (= count before insert)
+  int64_t position;    // t
+  int write_meta;      // 1 in exactly one launch of an insert
+};
+
+// Append (K_t, V_t, t, 1): copy each layer's block into the free slot
+// order[index] and record first = t, pos_sum = t, span = 1 (Sec. 3.3,
+// Alg. S1 Append).  grid.y = layer_in_launch * 2 + kv.
+__global__ __launch_bounds__(256) void insert_kernel(InsertArgs a) {
+  const int li = blockIdx.y >> 1;
+  const int kv = blockIdx.y & 1;
+  const int32_t* order = reinterpret_cast<const int32_t*>(a.pool + a.lay.off_order);
+  const int32_t slot = order[a.index];
+  const u32x4* src = reinterpret_cast<const u32x4*>(kv ? a.v[li] : a.k[li]);
+  u32x4* dst = reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, a.layer0 + li, slot, kv));
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t u = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < a.units; u += stride) {
+    __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
+  }
+  if (a.write_meta && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    int64_t* first = reinterpret_cast<int64_t*>(a.pool + a.lay.off_first);
+    int64_t* pos_sum = reinterpret_cast<int64_t*>(a.pool + a.lay.off_pos_sum);
+    int64_t* span = reinterpret_cast<int64_t*>(a.pool + a.lay.off_span);
+    first[a.index] = a.position;
+    pos_sum[a.index] = a.position;
+    span[a.index] = 1;
+  }
+}
+
+// Block-wide reductions for the 1024-thread schedule block.
+__device__ double block_min_f64(double v, double* red) {
+  for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o));
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    double x = (threadIdx.x < (blockDim.x >> 6)) ? red[threadIdx.x] : INFINITY;
+    for (int o = 32; o > 0; o >>= 1) x = fmin(x, __shfl_xor(x, o));
+    if (threadIdx.x == 0) red[0] = x;
+  }
+  __syncthreads();
+  double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__device__ int block_min_i32(int v, int* red) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    int x = (threadIdx.x < (blockDim.x >> 6)) ? red[threadIdx.x] : 0x7fffffff;
+    for (int o = 32; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
+    if (threadIdx.x == 0) red[0] = x;
+  }
+  __syncthreads();
+  int r = red[0];
+  __syncthreads();
+  return r;
+}
+
+// Distance-aware schedule and metadata consolidation for a memory holding
+// n = M+1 entries (Sec. 3.3 "Distance-aware scheduling" and "Consolidation
+// operator", Alg. S1).  One block of 1024 threads, thread i owns entry i.
+//   d_i = t - mu_i = (t*s_i - pos_sum_i) / s_i   (exact numerator, one fp64 division)
+//   u_i = d_i^beta
+//   g_i = |u_{i+1} - u_i| for the pairs i = 0..n-3 (the pair with the newest
+//         entry, n-2..n-1, is not eligible)
+//   j   = lowest i with g_i - min(g) <= 1e-9 * min(g)
+// Then splices the pair into one entry, frees the slot of entry j+1, and
+// writes the merge descriptor the merge kernel reads.
+__global__ __launch_bounds__(1024) void schedule_kernel(char* pool, Layout lay, int n, int64_t t,
+                                                        double beta, int anchor) {
+#pragma clang fp contract(off)
+  __shared__ double u_s[1024];
+  __shared__ int64_t f_s[1024], p_s[1024], s_s[1024];
+  __shared__ int32_t o_s[1024];
+  __shared__ double red_d[16];
+  __shared__ int red_i[16];
+
+  DevHeader* hdr = reinterpret_cast<DevHeader*>(pool);
+  int64_t* first = reinterpret_cast<int64_t*>(pool + lay.off_first);
+  int64_t* pos_sum = reinterpret_cast<int64_t*>(pool + lay.off_pos_sum);
+  int64_t* span = reinterpret_cast<int64_t*>(pool + lay.off_span);
+  int32_t* order = reinterpret_cast<int32_t*>(pool + lay.off_order);
+  int32_t* log = reinterpret_cast<int32_t*>(pool + lay.off_log);
+
+  const int i = threadIdx.x;
+  if (i < n) {
+    f_s[i] = first[i];
+    p_s[i] = pos_sum[i];
+    s_s[i] = span[i];
+    o_s[i] = order[i];
+  }
+  if (i < n - 1) {
+    const double d = double(t * s_s[i] - p_s[i]) / double(s_s[i]);
+    u_s[i] = (beta == 1.0) ? d : pow(d, beta);
+  }
+  __syncthreads();
+  const double g = (i < n - 2) ? fabs(u_s[i + 1] - u_s[i]) : INFINITY;
+  const double gm = block_min_f64(g, red_d);
+  const double tol = 1e-9 * gm;
+  const int cand = (i < n - 2 && (g - gm) <= tol) ? i : 0x7fffffff;
+  const int j = block_min_i32(cand, red_i);
+
+  const int64_t s_new = s_s[j] + s_s[j + 1];
+  const bool anchor_pair = anchor && j == 0;
+  const int64_t p_new = anchor_pair ? f_s[0] * s_new : p_s[j] + p_s[j + 1];
+  const int32_t freed = o_s[j + 1];
+
+  // Replace (m_j, m_{j+1}) by the merged entry; entries after the pair move
+  // one place toward the front; the freed slot goes to the end of order[].
+  if (i == j) {
+    pos_sum[i] = p_new;
+    span[i] = s_new;
+  } else if (i > j && i < n - 1) {
+    first[i] = f_s[i + 1];
+    pos_sum[i] = p_s[i + 1];
+    span[i] = s_s[i + 1];
+    order[i] = o_s[i + 1];
+  } else if (i == n - 1) {
+    order[i] = freed;
+  }
+  if (i == 0) {
+    const double rj = sqrt(double(s_s[j]));
+    const double rj1 = sqrt(double(s_s[j + 1]));
+    const double w_dst = rj / (rj + rj1);
+    hdr->desc_kind = anchor_pair ? kMergeAnchor : kMergeWeighted;
+    hdr->desc_dst_slot = o_s[j];
+    hdr->desc_src_slot = freed;
+    hdr->desc_w_dst = w_dst;
+    hdr->desc_w_src = 1.0 - w_dst;
+    const int64_t k = hdr->merges_total;
+    log[k % kLogCap] = j;
+    hdr->merges_total = k + 1;
+  }
+}
+
+// fp64 -> bf16 bits, round to nearest even: round to fp32 with
+// round-to-odd (truncate, then set the last bit if anything was dropped),
+// then fp32 -> bf16 to nearest even.  fp32 keeps 16 more bits than bf16,
+// so the two-step rounding equals a single correct rounding.
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double x) {
+  float f = __double2float_rz(x);
+  uint32_t b = __float_as_uint(f);
+  if (double(f) != x) b |= 1u;
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return b >> 16;
+}
+
+__device__ __forceinline__ double bf16_lo(uint32_t w) { return double(__uint_as_float(w << 16)); }
+__device__ __forceinline__ double bf16_hi(uint32_t w) { return double(__uint_as_float(w & 0xffff0000u)); }
+
+// K_new = w_j K_j + w_{j+1} K_{j+1} (same for V), each element in fp64 as two
+// products and one sum, rounded once to the storage type (Sec. 3.3
+// "Consolidation operator", Alg. S1).  In place into entry j's slot.
+// grid.y = layer * 2 + kv; a no-op unless the last schedule chose a
+// weighted pair.  Streaming: 16-byte nontemporal loads/stores, UNROLL
+// independent units in flight per thread.
+template <int UNROLL>
+__global__ __launch_bounds__(256) void merge_kernel_bf16(char* pool, Layout lay, int64_t units) {
+#pragma clang fp contract(off)
+  const DevHeader* hdr = reinterpret_cast<const DevHeader*>(pool);
+  if (hdr->desc_kind != kMergeWeighted) return;
+  const int layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const double wa = hdr->desc_w_dst, wb = hdr->desc_w_src;
+  u32x4* dst = reinterpret_cast<u32x4*>(pool + kv_offset(lay, layer, hdr->desc_dst_slot, kv));
+  const u32x4* src = reinterpret_cast<const u32x4*>(pool + kv_offset(lay, layer, hdr->desc_src_slot, kv));
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x * UNROLL;
+  for (int64_t base = int64_t(blockIdx.x) * blockDim.x * UNROLL + threadIdx.x; base < units; base += stride) {
+    u32x4 a[UNROLL], b[UNROLL];
+#pragma unroll
+    for (int r = 0; r < UNROLL; ++r) {
+      const int64_t u = base + int64_t(r) * blockDim.x;
+      if (u < units) {
+        a[r] = __builtin_nontemporal_load(dst + u);
+        b[r] = __builtin_nontemporal_load(src + u);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < UNROLL; ++r) {
+      const int64_t u = base + int64_t(r) * blockDim.x;
+      if (u < units) {
+        u32x4 o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const double lo = wa * bf16_lo(a[r][w]) + wb * bf16_lo(b[r][w]);
+          const double hi = wa * bf16_hi(a[r][w]) + wb * bf16_hi(b[r][w]);
+          o[w] = f64_to_bf16_rne(lo) | (f64_to_bf16_rne(hi) << 16);
+        }
+        __builtin_nontemporal_store(o, dst + u);
+      }
+    }
+  }
+}
+
+template <int UNROLL>
+__global__ __launch_bounds__(256) void merge_kernel_f32(char* pool, Layout lay, int64_t units) {
+#pragma clang fp contract(off)
+  const DevHeader* hdr = reinterpret_cast<const DevHeader*>(pool);
+  if (hdr->desc_kind != kMergeWeighted) return;
+  const int layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const double wa = hdr->desc_w_dst, wb = hdr->desc_w_src;
+  f32x4* dst = reinterpret_cast<f32x4*>(pool + kv_offset(lay, layer, hdr->desc_dst_slot, kv));
+  const f32x4* src = reinterpret_cast<const f32x4*>(pool + kv_offset(lay, layer, hdr->desc_src_slot, kv));
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x * UNROLL;
+  for (int64_t base = int64_t(blockIdx.x) * blockDim.x * UNROLL + threadIdx.x; base < units; base += stride) {
+    f32x4 a[UNROLL], b[UNROLL];
+#pragma unroll
+    for (int r = 0; r < UNROLL; ++r) {
+      const int64_t u = base + int64_t(r) * blockDim.x;
+      if (u < units) {
+        a[r] = __builtin_nontemporal_load(dst + u);
+        b[r] = __builtin_nontemporal_load(src + u);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < UNROLL; ++r) {
+      const int64_t u = base + int64_t(r) * blockDim.x;
+      if (u < units) {
+        f32x4 o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) o[w] = float(wa * double(a[r][w]) + wb * double(b[r][w]));
+        __builtin_nontemporal_store(o, dst + u);
+      }
+    }
+  }
+}
+
+constexpr int kMergeUnroll = 4;
+
+// Blocks per (layer, kv) plane for a streaming pass over `units` 16-byte
+// units, each thread taking `per_thread` of them.
+unsigned plane_blocks(int64_t units, int per_thread) {
+  int64_t threads = (units + per_thread - 1) / per_thread;
+  int64_t b = (threads + 255) / 256;
+  if (b < 1) b = 1;
+  if (b > 65535) b = 65535;
+  return unsigned(b);
+}
+
+bool valid_config(const fademem_config* c) {
+  if (!c) return false;
+  if (c->budget < 2 || c->budget > kMaxBudget) return false;
+  if (c->heads < 1 || c->heads > 4096) return false;
+  if (c->head_dim != 64 && c->head_dim != 128) return false;
+  if (c->tokens_per_block < 1 || c->tokens_per_block > kMaxTokens) return false;
+  if (!(c->beta > 0.0 && c->beta <= 1.0)) return false;
+  if (c->anchor != 0 && c->anchor != 1) return false;
+  if (c->dtype != FADEMEM_F32 && c->dtype != FADEMEM_BF16) return false;
+  if (c->layers < 1 || c->layers > 4096) return false;
+  return true;
+}
+
+}  // namespace
+
+namespace fademem {
+
+int compute_layout(const fademem_config* cfg, Layout* lay) {
+  if (!valid_config(cfg)) return FADEMEM_EINVAL;
+  Layout L{};
+  L.slots = cfg->budget + 1;
+  size_t off = round_up(sizeof(DevHeader), 256);
+  L.off_first = off;   off = round_up(off + 8 * size_t(L.slots), 256);
+  L.off_pos_sum = off; off = round_up(off + 8 * size_t(L.slots), 256);
+  L.off_span = off;    off = round_up(off + 8 * size_t(L.slots), 256);
+  L.off_order = off;   off = round_up(off + 4 * size_t(L.slots), 256);
+  L.off_log = off;     off = round_up(off + 4 * size_t(kLogCap), 256);
+  L.meta_bytes = off;
+  L.elt = cfg->dtype == FADEMEM_BF16 ? 2 : 4;
+  L.row_elems = size_t(cfg->heads) * size_t(cfg->head_dim);
+  const double blk = double(cfg->tokens_per_block) * double(L.row_elems) * double(L.elt);
+  if (blk > 1e15) return FADEMEM_EINVAL;
+  L.blk_bytes = size_t(cfg->tokens_per_block) * L.row_elems * L.elt;
+  L.blk_stride = round_up(L.blk_bytes, 256);
+  L.total = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
+  *lay = L;
+  return FADEMEM_OK;
+}
+
+}  // namespace fademem
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char* fademem_strerror(int code) {
+  switch (code) {
+    case FADEMEM_OK: return "ok";
+    case FADEMEM_EINVAL: return "invalid argument or configuration";
+    case FADEMEM_ESTATE: return "call not allowed in the current memory state";
+    case FADEMEM_ENOMEM: return "device pool too small";
+    case FADEMEM_EHIP: return "HIP runtime or launch error";
+    case FADEMEM_EUNSUPPORTED: return "not supported by this build";
+    default: return "unknown error";
+  }
+}
+
+int fademem_pool_bytes(const fademem_config* cfg, size_t* bytes) {
+  if (!bytes) return FADEMEM_EINVAL;
+  Layout L;
+  int rc = compute_layout(cfg, &L);
+  if (rc) return rc;
+  *bytes = L.total;
+  return FADEMEM_OK;
+}
+
+int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_bytes, void* stream,
+                         fademem_cache** out) {
+  if (!out) return FADEMEM_EINVAL;
+  *out = nullptr;
+  Layout L;
+  int rc = compute_layout(cfg, &L);
+  if (rc) return rc;
+  if (cfg->merge_op != FADEMEM_MERGE_SQRT_SPAN) return FADEMEM_EUNSUPPORTED;
+  if (!dev_pool || !aligned(dev_pool, 256)) return FADEMEM_EINVAL;
+  if (pool_bytes < L.total) return FADEMEM_ENOMEM;
+  fademem_cache* c = new (std::nothrow) fademem_cache();
+  if (!c) return FADEMEM_ENOMEM;
+  c->cfg = *cfg;
+  c->lay = L;
+  c->pool = static_cast<char*>(dev_pool);
+  c->count = 0;
+  c->newest = 0;
+  c->any_inserted = false;
+  c->last_hip_error = 0;
+  (void)hipGetLastError();
+  const unsigned blocks = unsigned((L.slots + 255) / 256);
+  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, as_stream(stream),
+                     reinterpret_cast<DevHeader*>(c->pool), reinterpret_cast<int32_t*>(c->pool + L.off_order),
+                     L.slots);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    int err = int(e);
+    delete c;
+    (void)err;
+    return FADEMEM_EHIP;
+  }
+  *out = c;
+  return FADEMEM_OK;
+}
+
+int fademem_cache_destroy(fademem_cache* cache) {
+  delete cache;
+  return FADEMEM_OK;
+}
+
+int fademem_count(const fademem_cache* cache, int64_t* count) {
+  if (!cache || !count) return FADEMEM_EINVAL;
+  *count = cache->count;
+  return FADEMEM_OK;
+}
+
+int fademem_last_hip_error(const fademem_cache* cache) { return cache ? cache->last_hip_error : 0; }
+
+int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v, int64_t position, void* stream) {
+  if (!c || !k || !v) return FADEMEM_EINVAL;
+  if (position <= -kMaxPosition || position >= kMaxPosition) return FADEMEM_EINVAL;
+  const int layers = c->cfg.layers;
+  for (int l = 0; l < layers; ++l) {
+    if (!k[l] || !v[l] || !aligned(k[l], 16) || !aligned(v[l], 16)) return FADEMEM_EINVAL;
+  }
+  if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
+  if (c->any_inserted && position <= c->newest) return FADEMEM_ESTATE;
+  (void)hipGetLastError();
+  const int64_t units = int64_t(c->lay.blk_bytes / 16);
+  for (int l0 = 0; l0 < layers; l0 += kMaxLayersPerLaunch) {
+    const int nl = (layers - l0) < kMaxLayersPerLaunch ? (layers - l0) : kMaxLayersPerLaunch;
+    InsertArgs a;
+    memset(&a, 0, sizeof(a));
+    for (int l = 0; l < nl; ++l) {
+      a.k[l] = k[l0 + l];
+      a.v[l] = v[l0 + l];
+    }
+    a.pool = c->pool;
+    a.lay = c->lay;
+    a.layer0 = l0;
+    a.units = units;
+    a.index = c->count;
+    a.position = position;
+    a.write_meta = (l0 == 0);
+    hipLaunchKernelGGL(insert_kernel, dim3(plane_blocks(units, 4), unsigned(2 * nl)), dim3(256), 0,
+                       as_stream(stream), a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(c, e);
+  }
+  c->count += 1;
+  c->newest = position;
+  c->any_inserted = true;
+  return FADEMEM_OK;
+}
+
+int fademem_consolidate(fademem_cache* c, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (c->count <= c->cfg.budget) return FADEMEM_OK;  // Alg. S1: within budget, nothing to do
+  (void)hipGetLastError();
+  const int n = int(c->count);
+  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(1024), 0, as_stream(stream), c->pool, c->lay, n, c->newest,
+                     c->cfg.beta, c->cfg.anchor);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(c, e);
+  const int64_t units = int64_t(c->lay.blk_bytes / 16);
+  const dim3 grid(plane_blocks(units, kMergeUnroll), unsigned(2 * c->cfg.layers));
+  if (c->cfg.dtype == FADEMEM_BF16) {
+    hipLaunchKernelGGL(merge_kernel_bf16<kMergeUnroll>, grid, dim3(256), 0, as_stream(stream), c->pool, c->lay,
+                       units);
+  } else {
+    hipLaunchKernelGGL(merge_kernel_f32<kMergeUnroll>, grid, dim3(256), 0, as_stream(stream), c->pool, c->lay,
+                       units);
+  }
+  e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(c, e);
+  c->count -= 1;
+  return FADEMEM_OK;
+}
+
+int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, const void* k_cur,
+                   const void* v_cur, int64_t cur_tokens, float scale, void* out, float* lse, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (layer < 0 || layer >= c->cfg.layers) return FADEMEM_EINVAL;
+  if (q_tokens < 0 || q_tokens > kMaxTokens || cur_tokens < 0 || cur_tokens > kMaxTokens) return FADEMEM_EINVAL;
+  if (q_tokens == 0) return FADEMEM_OK;
+  if (!q || !out || !aligned(q, 16) || !aligned(out, 16)) return FADEMEM_EINVAL;
+  if (lse && !aligned(lse, 4)) return FADEMEM_EINVAL;
+  if (cur_tokens > 0 && (!k_cur || !v_cur || !aligned(k_cur, 16) || !aligned(v_cur, 16))) return FADEMEM_EINVAL;
+  if (c->count == 0 && cur_tokens == 0) return FADEMEM_EINVAL;  // no keys at all
+  const double total_keys = double(c->count) * double(c->cfg.tokens_per_block) + double(cur_tokens);
+  if (total_keys > double(kMaxTokens)) return FADEMEM_EINVAL;
+  if (!(scale >= 0.0f) || isinf(scale)) return FADEMEM_EINVAL;
+  AttendArgs a;
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.kv_layer_base = c->pool + kv_offset(c->lay, layer, 0, 0);
+  a.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order);
+  a.k_cur = k_cur;
+  a.v_cur = v_cur;
+  a.n_entries = c->count;
+  a.tokens_per_block = c->cfg.tokens_per_block;
+  a.cur_tokens = cur_tokens;
+  a.q_tokens = q_tokens;
+  a.slot_stride = 2 * c->lay.blk_stride;
+  a.v_offset = c->lay.blk_stride;
+  a.heads = c->cfg.heads;
+  a.head_dim = c->cfg.head_dim;
+  a.scale = scale > 0.0f ? scale : 1.0f / sqrtf(float(c->cfg.head_dim));
+  (void)hipGetLastError();
+  hipError_t e = (c->cfg.dtype == FADEMEM_BF16) ? launch_attend_bf16(a, as_stream(stream))
+                                                : launch_attend_f32(a, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  return FADEMEM_OK;
+}
+
+int fademem_get_state(fademem_cache* c, int64_t* count, int64_t* first, int64_t* span, int64_t* pos_sum,
+                      int64_t* newest, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  const size_t n = size_t(c->count);
+  if (count) *count = c->count;
+  if (newest) *newest = c->any_inserted ? c->newest : 0;
+  struct Item { int64_t* dst; size_t off; } items[3] = {{first, c->lay.off_first}, {span, c->lay.off_span},
+                                                        {pos_sum, c->lay.off_pos_sum}};
+  for (const Item& it : items) {
+    if (it.dst && n > 0) {
+      e = hipMemcpy(it.dst, c->pool + it.off, n * sizeof(int64_t), hipMemcpyDeviceToHost);
+      if (e != hipSuccess) return hip_fail(c, e);
+    }
+  }
+  return FADEMEM_OK;
+}
+
+int fademem_entry_kv(fademem_cache* c, int32_t layer, int64_t i, const void** k, const void** v, void* stream) {
+  if (!c || !k || !v) return FADEMEM_EINVAL;
+  if (layer < 0 || layer >= c->cfg.layers || i < 0 || i >= c->count) return FADEMEM_EINVAL;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  int32_t slot = 0;
+  e = hipMemcpy(&slot, c->pool + c->lay.off_order + 4 * size_t(i), sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e);
+  *k = c->pool + kv_offset(c->lay, layer, slot, 0);
+  *v = c->pool + kv_offset(c->lay, layer, slot, 1);
+  return FADEMEM_OK;
+}
+
+int fademem_merge_log(fademem_cache* c, int32_t* j, int64_t cap, int64_t* total, void* stream) {
+  if (!c || !total || cap < 0 || (cap > 0 && !j)) return FADEMEM_EINVAL;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  DevHeader h;
+  e = hipMemcpy(&h, c->pool, sizeof(h), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e);
+  *total = h.merges_total;
+  int64_t keep = h.merges_total;
+  if (keep > kLogCap) keep = kLogCap;
+  if (keep > cap) keep = cap;
+  if (keep == 0) return FADEMEM_OK;
+  int32_t ring[kLogCap];
+  e = hipMemcpy(ring, c->pool + c->lay.off_log, sizeof(ring), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e);
+  for (int64_t r = 0; r < keep; ++r) {
+    const int64_t idx = h.merges_total - keep + r;
+    j[r] = ring[idx % kLogCap];
+  }
+  return FADEMEM_OK;
+}
+
+}  // extern "C"

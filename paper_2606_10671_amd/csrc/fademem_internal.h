@@ -1,0 +1,85 @@
+// Internal declarations shared by the translation units of libfademem.so.
+// Not part of the public interface (include/fademem.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fademem.h"
+
+namespace fademem {
+
+constexpr int kLogCap = 4096;             // merge-log ring capacity (entries)
+constexpr int64_t kMaxBudget = 1023;      // schedule runs in one 1024-thread block
+constexpr int kMaxLayersPerLaunch = 64;   // layer pointers passed as kernel arguments
+constexpr int64_t kMaxPosition = int64_t(1) << 40;
+constexpr int64_t kMaxTokens = int64_t(1) << 30;
+
+enum MergeKind : int32_t { kMergeNone = 0, kMergeWeighted = 1, kMergeAnchor = 2 };
+
+// Device-resident header at the start of the pool.  Written only by the
+// library's kernels; the host reads it back for get_state / merge_log.
+struct DevHeader {
+  int64_t merges_total;   // consolidations run (length of the merge log)
+  int32_t desc_kind;      // MergeKind of the most recent consolidation
+  int32_t desc_dst_slot;  // slot of entry j (receives the merged block)
+  int32_t desc_src_slot;  // slot of entry j+1 (freed)
+  int32_t pad0;
+  double desc_w_dst;      // w_j
+  double desc_w_src;      // w_{j+1}
+};
+
+// Pool layout.  Metadata arrays are indexed by logical entry (0 = oldest);
+// order[] maps logical entry -> KV slot.  order[] is a permutation of
+// 0..M, its first `count` elements are the live entries' slots and the rest
+// are free slots, so compaction never moves KV.
+struct Layout {
+  int64_t slots;       // M + 1
+  size_t off_first;    // int64[slots]
+  size_t off_pos_sum;  // int64[slots]
+  size_t off_span;     // int64[slots]
+  size_t off_order;    // int32[slots]
+  size_t off_log;      // int32[kLogCap]
+  size_t meta_bytes;   // multiple of 256
+  size_t elt;          // bytes per element
+  size_t blk_bytes;    // N*H*D*elt: one K (or V) block
+  size_t blk_stride;   // blk_bytes rounded up to 256
+  size_t row_elems;    // H*D: elements per token row
+  size_t total;        // meta_bytes + layers*slots*2*blk_stride
+};
+
+int compute_layout(const fademem_config* cfg, Layout* lay);
+
+// Address of layer l, slot s, kind kv (0 = K, 1 = V) inside the KV region.
+__host__ __device__ inline size_t kv_offset(const Layout& lay, int64_t layer, int64_t slot, int kv) {
+  return lay.meta_bytes + ((size_t(layer) * lay.slots + size_t(slot)) * 2 + kv) * lay.blk_stride;
+}
+
+// Attention launchers (attend_bf16.hip, attend_f32.hip).  All pointers are
+// device pointers; `entry_k0` is layer's KV region base (slot 0, K) and the
+// slot of logical entry e is order[e]; slot s's K block starts at
+// entry_k0 + s*2*blk_stride bytes and its V block blk_stride bytes later.
+struct AttendArgs {
+  const void* q;
+  void* out;
+  float* lse;
+  const char* kv_layer_base;  // pool + kv_offset(layer, 0, 0)
+  const int32_t* order;       // logical -> slot
+  const void* k_cur;
+  const void* v_cur;
+  int64_t n_entries;          // entries exposed from memory
+  int64_t tokens_per_block;   // N
+  int64_t cur_tokens;         // rows of the current chunk
+  int64_t q_tokens;
+  size_t slot_stride;         // bytes between consecutive slots' K blocks (2*blk_stride)
+  size_t v_offset;            // bytes from a slot's K block to its V block
+  int heads;
+  int head_dim;
+  float scale;
+};
+
+hipError_t launch_attend_bf16(const AttendArgs& a, hipStream_t stream);
+hipError_t launch_attend_f32(const AttendArgs& a, hipStream_t stream);
+
+}  // namespace fademem

@@ -1,0 +1,80 @@
+"""GPU parity of the bf16 path at sizes the oracle runs in seconds, spanning
+several 64-key tiles, 128-query tiles and ragged tails.
+
+Each chunk: attention of the chunk's queries over [memory || chunk] (Sec.
+3.1, Sec. 4.1), then one Alg. S1 update per frame.  Schedule state, merge
+log and every stored K/V entry are compared bit for bit; attention output
+within 2e-2 max-abs, 1e-2 normwise and 2e-3 LSE of the fp64 oracle."""
+import numpy as np
+import pytest
+
+from oracle import OracleCache
+from paper_2606_10671_amd.synth import NumpyWanStream
+
+from parity import check_attention, check_entries, check_state, oracle_attend, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def run_chunks(H, D, N, F, M, chunks, beta=0.3, anchor=True, layers=1, q_scale=1.0, seed=0,
+               check_every_entry=True):
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    print(f"bf16 run H={H} D={D} N={N} F={F} M={M} chunks={chunks} beta={beta} anchor={anchor} "
+          f"layers={layers} q_scale={q_scale}", flush=True)
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=beta, anchor=anchor,
+                  dtype=torch.bfloat16, layers=layers)
+    ocs = [OracleCache(budget=M, beta=beta, anchor=anchor, storage="bf16") for _ in range(layers)]
+    streams = [NumpyWanStream(seed + 101 * l, N, H, D) for l in range(layers)]
+    worst = [0.0, 0.0, 0.0]
+    for c in range(chunks):
+        frames = [[s.frame() for _ in range(F)] for s in streams]
+        for l in range(layers):
+            q = streams[l].queries(F * N) * np.float32(q_scale)
+            K = np.concatenate([f[0] for f in frames[l]])
+            V = np.concatenate([f[1] for f in frames[l]])
+            qd, kd, vd = (torch.from_numpy(np.ascontiguousarray(x)).to("cuda", torch.bfloat16) for x in (q, K, V))
+            lse = torch.empty((H, F * N), dtype=torch.float32, device="cuda")
+            out = cache.attend(qd, kd, vd, layer=l, lse=lse)
+            O_ref, L_ref = oracle_attend(ocs[l], q, K, V)
+            errs = check_attention(to_np(out), to_np(lse), O_ref, L_ref, "bf16", where=(c, l))
+            worst = [max(a, b) for a, b in zip(worst, errs)]
+        for f in range(F):
+            kf = [torch.from_numpy(frames[l][f][0]).to("cuda", torch.bfloat16) for l in range(layers)]
+            vf = [torch.from_numpy(frames[l][f][1]).to("cuda", torch.bfloat16) for l in range(layers)]
+            cache.insert(kf, vf, c * F + f)
+            cache.consolidate()
+            for l in range(layers):
+                ocs[l].update(frames[l][f][0], frames[l][f][1], c * F + f)
+        check_state(cache, ocs[0], where=c)
+        if check_every_entry or c == chunks - 1:
+            for l in range(layers):
+                check_entries(cache, ocs[l], layer=l, where=(c, l))
+    total, log = cache.merge_log()
+    assert log == ocs[0].merge_log[-len(log):] and total == len(ocs[0].merge_log)
+    print(f"worst max-abs {worst[0]:.3e} normwise {worst[1]:.3e} lse {worst[2]:.3e}", flush=True)
+    return cache, ocs
+
+
+def test_bf16_d128_ragged():
+    # N = 200 rows per entry: tiles straddle entries; F*N = 600 queries = 4 tiles + 88 rows.
+    run_chunks(H=2, D=128, N=200, F=3, M=6, chunks=8)
+
+
+def test_bf16_d64_anchor_off_beta1_ties():
+    run_chunks(H=3, D=64, N=72, F=2, M=5, chunks=10, beta=1.0, anchor=False)
+
+
+def test_bf16_layers_share_one_schedule():
+    run_chunks(H=1, D=128, N=96, F=3, M=4, chunks=5, layers=3, beta=0.5)
+
+
+def test_bf16_peaked_softmax():
+    # Queries scaled x8: softmax is dominated by few keys, so a dropped or
+    # misplaced cache row shows up as a large error.
+    run_chunks(H=2, D=128, N=130, F=3, M=4, chunks=5, q_scale=8.0)
+
+
+def test_bf16_wan_heads_small_tokens():
+    # Wan-class head layout (12 x 128) with few tokens per frame.
+    run_chunks(H=12, D=128, N=64, F=3, M=21, chunks=10, check_every_entry=False)
