@@ -19,6 +19,8 @@ struct fademem_cache {
   char* pool;
   int64_t count;        // entries held (mirrors the device state exactly)
   int64_t newest;       // newest inserted position
+  int64_t inserted;     // blocks inserted so far
+  int cur;              // metadata copy holding the current state (0 or 1)
   bool any_inserted;
   int last_hip_error;
 };
@@ -39,23 +41,38 @@ inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s);
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Typed views of one metadata copy.
+struct Meta {
+  int64_t* first;
+  int64_t* pos_sum;
+  int64_t* span;
+  int32_t* order;
+};
+__host__ __device__ inline Meta meta_of(char* pool, const Layout& lay, int copy) {
+  Meta m;
+  m.first = reinterpret_cast<int64_t*>(pool + lay.off_first[copy]);
+  m.pos_sum = reinterpret_cast<int64_t*>(pool + lay.off_pos_sum[copy]);
+  m.span = reinterpret_cast<int64_t*>(pool + lay.off_span[copy]);
+  m.order = reinterpret_cast<int32_t*>(pool + lay.off_order[copy]);
+  return m;
+}
+
 // ---------------------------------------------------------------------------
 // Kernels
 // ---------------------------------------------------------------------------
 
-// Empty memory: order = identity permutation, counters cleared.
-__global__ void init_kernel(DevHeader* hdr, int32_t* order, int64_t slots) {
-  int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+// Empty memory: both order copies = identity permutation, counters cleared.
+__global__ void init_kernel(char* pool, Layout lay) {
+  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i == 0) {
+    DevHeader* hdr = reinterpret_cast<DevHeader*>(pool);
     hdr->merges_total = 0;
-    hdr->desc_kind = kMergeNone;
-    hdr->desc_dst_slot = 0;
-    hdr->desc_src_slot = 0;
-    hdr->pad0 = 0;
-    hdr->desc_w_dst = 0.0;
-    hdr->desc_w_src = 0.0;
+    hdr->anchor_merges = 0;
   }
-  if (i < slots) order[i] = int32_t(i);
+  if (i < lay.slots) {
+    meta_of(pool, lay, 0).order[i] = int32_t(i);
+    meta_of(pool, lay, 1).order[i] = int32_t(i);
+  }
 }
 
 struct InsertArgs {
@@ -67,6 +84,7 @@ struct InsertArgs {
   int64_t units;       // 16-byte units per block
   int64_t index;       // logical index of the new entry (= count before insert)
   int64_t position;    // t
+  int cur;             // current metadata copy
   int write_meta;      // 1 in exactly one launch of an insert
 };
 
@@ -76,8 +94,8 @@ struct InsertArgs {
 __global__ __launch_bounds__(256) void insert_kernel(InsertArgs a) {
   const int li = blockIdx.y >> 1;
   const int kv = blockIdx.y & 1;
-  const int32_t* order = reinterpret_cast<const int32_t*>(a.pool + a.lay.off_order);
-  const int32_t slot = order[a.index];
+  const Meta m = meta_of(a.pool, a.lay, a.cur);
+  const int32_t slot = m.order[a.index];
   const u32x4* src = reinterpret_cast<const u32x4*>(kv ? a.v[li] : a.k[li]);
   u32x4* dst = reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, a.layer0 + li, slot, kv));
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
@@ -85,28 +103,19 @@ __global__ __launch_bounds__(256) void insert_kernel(InsertArgs a) {
     __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
   }
   if (a.write_meta && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
-    int64_t* first = reinterpret_cast<int64_t*>(a.pool + a.lay.off_first);
-    int64_t* pos_sum = reinterpret_cast<int64_t*>(a.pool + a.lay.off_pos_sum);
-    int64_t* span = reinterpret_cast<int64_t*>(a.pool + a.lay.off_span);
-    first[a.index] = a.position;
-    pos_sum[a.index] = a.position;
-    span[a.index] = 1;
+    m.first[a.index] = a.position;
+    m.pos_sum[a.index] = a.position;
+    m.span[a.index] = 1;
   }
 }
 
-// Block-wide reductions for the 1024-thread schedule block.
+// Block-wide reductions for 256-thread blocks (4 waves).
 __device__ double block_min_f64(double v, double* red) {
   for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o));
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (lane == 0) red[w] = v;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    double x = (threadIdx.x < (blockDim.x >> 6)) ? red[threadIdx.x] : INFINITY;
-    for (int o = 32; o > 0; o >>= 1) x = fmin(x, __shfl_xor(x, o));
-    if (threadIdx.x == 0) red[0] = x;
-  }
-  __syncthreads();
-  double r = red[0];
+  double r = fmin(fmin(red[0], red[1]), fmin(red[2], red[3]));
   __syncthreads();
   return r;
 }
@@ -116,180 +125,179 @@ __device__ int block_min_i32(int v, int* red) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (lane == 0) red[w] = v;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    int x = (threadIdx.x < (blockDim.x >> 6)) ? red[threadIdx.x] : 0x7fffffff;
-    for (int o = 32; o > 0; o >>= 1) x = min(x, __shfl_xor(x, o));
-    if (threadIdx.x == 0) red[0] = x;
-  }
-  __syncthreads();
-  int r = red[0];
+  int r = min(min(red[0], red[1]), min(red[2], red[3]));
   __syncthreads();
   return r;
 }
 
-// Distance-aware schedule and metadata consolidation for a memory holding
-// n = M+1 entries (Sec. 3.3 "Distance-aware scheduling" and "Consolidation
-// operator", Alg. S1).  One block of 1024 threads, thread i owns entry i.
-//   d_i = t - mu_i = (t*s_i - pos_sum_i) / s_i   (exact numerator, one fp64 division)
-//   u_i = d_i^beta
-//   g_i = |u_{i+1} - u_i| for the pairs i = 0..n-3 (the pair with the newest
-//         entry, n-2..n-1, is not eligible)
-//   j   = lowest i with g_i - min(g) <= 1e-9 * min(g)
-// Then splices the pair into one entry, frees the slot of entry j+1, and
-// writes the merge descriptor the merge kernel reads.
-__global__ __launch_bounds__(1024) void schedule_kernel(char* pool, Layout lay, int n, int64_t t,
-                                                        double beta, int anchor) {
-#pragma clang fp contract(off)
-  __shared__ double u_s[1024];
-  __shared__ int64_t f_s[1024], p_s[1024], s_s[1024];
-  __shared__ int32_t o_s[1024];
-  __shared__ double red_d[16];
-  __shared__ int red_i[16];
-
-  DevHeader* hdr = reinterpret_cast<DevHeader*>(pool);
-  int64_t* first = reinterpret_cast<int64_t*>(pool + lay.off_first);
-  int64_t* pos_sum = reinterpret_cast<int64_t*>(pool + lay.off_pos_sum);
-  int64_t* span = reinterpret_cast<int64_t*>(pool + lay.off_span);
-  int32_t* order = reinterpret_cast<int32_t*>(pool + lay.off_order);
-  int32_t* log = reinterpret_cast<int32_t*>(pool + lay.off_log);
-
-  const int i = threadIdx.x;
-  if (i < n) {
-    f_s[i] = first[i];
-    p_s[i] = pos_sum[i];
-    s_s[i] = span[i];
-    o_s[i] = order[i];
-  }
-  if (i < n - 1) {
-    const double d = double(t * s_s[i] - p_s[i]) / double(s_s[i]);
-    u_s[i] = (beta == 1.0) ? d : pow(d, beta);
-  }
-  __syncthreads();
-  const double g = (i < n - 2) ? fabs(u_s[i + 1] - u_s[i]) : INFINITY;
-  const double gm = block_min_f64(g, red_d);
-  const double tol = 1e-9 * gm;
-  const int cand = (i < n - 2 && (g - gm) <= tol) ? i : 0x7fffffff;
-  const int j = block_min_i32(cand, red_i);
-
-  const int64_t s_new = s_s[j] + s_s[j + 1];
-  const bool anchor_pair = anchor && j == 0;
-  const int64_t p_new = anchor_pair ? f_s[0] * s_new : p_s[j] + p_s[j + 1];
-  const int32_t freed = o_s[j + 1];
-
-  // Replace (m_j, m_{j+1}) by the merged entry; entries after the pair move
-  // one place toward the front; the freed slot goes to the end of order[].
-  if (i == j) {
-    pos_sum[i] = p_new;
-    span[i] = s_new;
-  } else if (i > j && i < n - 1) {
-    first[i] = f_s[i + 1];
-    pos_sum[i] = p_s[i + 1];
-    span[i] = s_s[i + 1];
-    order[i] = o_s[i + 1];
-  } else if (i == n - 1) {
-    order[i] = freed;
-  }
-  if (i == 0) {
-    const double rj = sqrt(double(s_s[j]));
-    const double rj1 = sqrt(double(s_s[j + 1]));
-    const double w_dst = rj / (rj + rj1);
-    hdr->desc_kind = anchor_pair ? kMergeAnchor : kMergeWeighted;
-    hdr->desc_dst_slot = o_s[j];
-    hdr->desc_src_slot = freed;
-    hdr->desc_w_dst = w_dst;
-    hdr->desc_w_src = 1.0 - w_dst;
-    const int64_t k = hdr->merges_total;
-    log[k % kLogCap] = j;
-    hdr->merges_total = k + 1;
-  }
+// fp64 -> fp32 with round-to-odd: the hardware conversion rounds to
+// nearest; if that moved away from zero, step back one ulp (truncation),
+// then set the last bit when the conversion was inexact.  Rounding the
+// result to bf16 to nearest even then equals a single correct rounding of
+// x to bf16, because fp32 carries 16 more significand bits than bf16.
+__device__ __forceinline__ float f64_to_f32_odd(double x) {
+  const float f = float(x);
+  const double xd = double(f);
+  uint32_t b = __float_as_uint(f);
+  b -= (fabs(xd) > fabs(x)) ? 1u : 0u;
+  b |= (xd != x) ? 1u : 0u;
+  return __uint_as_float(b);
 }
 
-// fp64 -> bf16 bits, round to nearest even: round to fp32 with
-// round-to-odd (truncate, then set the last bit if anything was dropped),
-// then fp32 -> bf16 to nearest even.  fp32 keeps 16 more bits than bf16,
-// so the two-step rounding equals a single correct rounding.
-__device__ __forceinline__ uint32_t f64_to_bf16_rne(double x) {
-  float f = __double2float_rz(x);
-  uint32_t b = __float_as_uint(f);
-  if (double(f) != x) b |= 1u;
-  b += 0x7fffu + ((b >> 16) & 1u);
-  return b >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp64 values -> packed bf16x2 (low half = lo), each rounded to nearest even.
+__device__ __forceinline__ uint32_t pack_bf16_rne(double lo, double hi) {
+  bf16x2_t v;
+  v[0] = (__bf16)f64_to_f32_odd(lo);
+  v[1] = (__bf16)f64_to_f32_odd(hi);
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 __device__ __forceinline__ double bf16_lo(uint32_t w) { return double(__uint_as_float(w << 16)); }
 __device__ __forceinline__ double bf16_hi(uint32_t w) { return double(__uint_as_float(w & 0xffff0000u)); }
 
-// K_new = w_j K_j + w_{j+1} K_{j+1} (same for V), each element in fp64 as two
-// products and one sum, rounded once to the storage type (Sec. 3.3
-// "Consolidation operator", Alg. S1).  In place into entry j's slot.
-// grid.y = layer * 2 + kv; a no-op unless the last schedule chose a
-// weighted pair.  Streaming: 16-byte nontemporal loads/stores, UNROLL
-// independent units in flight per thread.
-template <int UNROLL>
-__global__ __launch_bounds__(256) void merge_kernel_bf16(char* pool, Layout lay, int64_t units) {
+struct ConsolidateArgs {
+  char* pool;
+  Layout lay;
+  int n;            // entries held (M + 1)
+  int layers;
+  int64_t t;        // newest position
+  double beta;
+  int anchor;
+  int cur;          // metadata copy read; the other copy is written
+  int64_t units;    // 16-byte units per K (or V) block
+};
+
+// One consolidation (Sec. 3.3 "Distance-aware scheduling" and
+// "Consolidation operator", Alg. S1) in one launch.  Every block derives
+// the decision from the current metadata copy, which no block writes:
+//   d_i = t - mu_i = (t*s_i - pos_sum_i) / s_i   (exact numerator, one fp64 division)
+//   u_i = d_i^beta
+//   g_i = |u_{i+1} - u_i| for the pairs i = 0..n-3 (the pair holding the
+//         newest entry, n-2..n-1, is not eligible)
+//   j   = lowest i with g_i - min(g) <= 1e-9 * min(g)
+// Block 0 writes the spliced metadata into the other copy (spans add,
+// pos_sum adds so mu is span-weighted; the anchor keeps its position, the
+// slot of entry j+1 is freed) and appends j to the merge log.  Unless the
+// pair holds the anchor, all blocks then merge entry j+1 into entry j's
+// slot: X_new = w_j X_j + w_{j+1} X_{j+1}, each element in fp64 as two
+// products and one sum, rounded once to the storage type.  The blocks of
+// each (layer, K|V) plane stride over it with 16-byte nontemporal
+// loads/stores, UNROLL units in flight per thread; grid.y = layer * 2 + kv.
+template <bool BF16, int UNROLL>
+__global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
 #pragma clang fp contract(off)
-  const DevHeader* hdr = reinterpret_cast<const DevHeader*>(pool);
-  if (hdr->desc_kind != kMergeWeighted) return;
-  const int layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
-  const double wa = hdr->desc_w_dst, wb = hdr->desc_w_src;
-  u32x4* dst = reinterpret_cast<u32x4*>(pool + kv_offset(lay, layer, hdr->desc_dst_slot, kv));
-  const u32x4* src = reinterpret_cast<const u32x4*>(pool + kv_offset(lay, layer, hdr->desc_src_slot, kv));
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x * UNROLL;
-  for (int64_t base = int64_t(blockIdx.x) * blockDim.x * UNROLL + threadIdx.x; base < units; base += stride) {
-    u32x4 a[UNROLL], b[UNROLL];
-#pragma unroll
-    for (int r = 0; r < UNROLL; ++r) {
-      const int64_t u = base + int64_t(r) * blockDim.x;
-      if (u < units) {
-        a[r] = __builtin_nontemporal_load(dst + u);
-        b[r] = __builtin_nontemporal_load(src + u);
+  __shared__ double u_s[kMaxBudget + 1];
+  __shared__ double g_s[kMaxBudget + 1];
+  __shared__ double red_d[4];
+  __shared__ int red_i[4];
+
+  const Meta m = meta_of(a.pool, a.lay, a.cur);
+  const int n = a.n;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < n - 1; i += 256) {
+    const int64_t s = m.span[i];
+    const double d = double(a.t * s - m.pos_sum[i]) / double(s);
+    u_s[i] = (a.beta == 1.0) ? d : pow(d, a.beta);
+  }
+  __syncthreads();
+  double gmin = INFINITY;
+  for (int i = tid; i < n - 2; i += 256) {
+    const double g = fabs(u_s[i + 1] - u_s[i]);
+    g_s[i] = g;
+    gmin = fmin(gmin, g);
+  }
+  const double gm = block_min_f64(gmin, red_d);
+  const double tol = 1e-9 * gm;
+  int cand = 0x7fffffff;
+  for (int i = tid; i < n - 2; i += 256) {
+    if (g_s[i] - gm <= tol) cand = min(cand, i);
+  }
+  const int j = block_min_i32(cand, red_i);
+
+  const int64_t s_j = m.span[j], s_j1 = m.span[j + 1];
+  const bool anchor_pair = a.anchor && j == 0;
+  const int32_t dst_slot = m.order[j];
+  const int32_t src_slot = m.order[j + 1];
+
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    const Meta w = meta_of(a.pool, a.lay, a.cur ^ 1);
+    for (int i = tid; i < n; i += 256) {
+      if (i < j) {
+        w.first[i] = m.first[i];
+        w.pos_sum[i] = m.pos_sum[i];
+        w.span[i] = m.span[i];
+        w.order[i] = m.order[i];
+      } else if (i == j) {
+        const int64_t s_new = s_j + s_j1;
+        w.first[i] = m.first[j];
+        w.pos_sum[i] = anchor_pair ? m.first[j] * s_new : m.pos_sum[j] + m.pos_sum[j + 1];
+        w.span[i] = s_new;
+        w.order[i] = dst_slot;
+      } else if (i < n - 1) {
+        w.first[i] = m.first[i + 1];
+        w.pos_sum[i] = m.pos_sum[i + 1];
+        w.span[i] = m.span[i + 1];
+        w.order[i] = m.order[i + 1];
+      } else {
+        w.order[i] = src_slot;  // freed slot
       }
     }
-#pragma unroll
-    for (int r = 0; r < UNROLL; ++r) {
-      const int64_t u = base + int64_t(r) * blockDim.x;
-      if (u < units) {
-        u32x4 o;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const double lo = wa * bf16_lo(a[r][w]) + wb * bf16_lo(b[r][w]);
-          const double hi = wa * bf16_hi(a[r][w]) + wb * bf16_hi(b[r][w]);
-          o[w] = f64_to_bf16_rne(lo) | (f64_to_bf16_rne(hi) << 16);
-        }
-        __builtin_nontemporal_store(o, dst + u);
-      }
+    // order[] keeps all M+1 slots: copy the free tail beyond the held entries.
+    for (int i = n + tid; i < a.lay.slots; i += 256) w.order[i] = m.order[i];
+    if (tid == 0) {
+      DevHeader* hdr = reinterpret_cast<DevHeader*>(a.pool);
+      int32_t* log = reinterpret_cast<int32_t*>(a.pool + a.lay.off_log);
+      const int64_t k = hdr->merges_total;
+      log[k % kLogCap] = j;
+      hdr->merges_total = k + 1;
+      if (anchor_pair) hdr->anchor_merges += 1;
     }
   }
-}
+  if (anchor_pair) return;  // the anchor keeps its K and V; nothing to move
 
-template <int UNROLL>
-__global__ __launch_bounds__(256) void merge_kernel_f32(char* pool, Layout lay, int64_t units) {
-#pragma clang fp contract(off)
-  const DevHeader* hdr = reinterpret_cast<const DevHeader*>(pool);
-  if (hdr->desc_kind != kMergeWeighted) return;
-  const int layer = blockIdx.y >> 1, kv = blockIdx.y & 1;
-  const double wa = hdr->desc_w_dst, wb = hdr->desc_w_src;
-  f32x4* dst = reinterpret_cast<f32x4*>(pool + kv_offset(lay, layer, hdr->desc_dst_slot, kv));
-  const f32x4* src = reinterpret_cast<const f32x4*>(pool + kv_offset(lay, layer, hdr->desc_src_slot, kv));
-  const int64_t stride = int64_t(gridDim.x) * blockDim.x * UNROLL;
-  for (int64_t base = int64_t(blockIdx.x) * blockDim.x * UNROLL + threadIdx.x; base < units; base += stride) {
-    f32x4 a[UNROLL], b[UNROLL];
+  const double rj = sqrt(double(s_j));
+  const double rj1 = sqrt(double(s_j1));
+  const double wa = rj / (rj + rj1);
+  const double wb = 1.0 - wa;
+  const int64_t step = int64_t(gridDim.x) * 256 * UNROLL;
+  {
+    const int plane = blockIdx.y;  // layer * 2 + kv
+    const int layer = plane >> 1, kv = plane & 1;
+    u32x4* dst = reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, layer, dst_slot, kv));
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.pool + kv_offset(a.lay, layer, src_slot, kv));
+    for (int64_t base = int64_t(blockIdx.x) * 256 * UNROLL + tid; base < a.units; base += step) {
+      u32x4 x[UNROLL], y[UNROLL];
 #pragma unroll
-    for (int r = 0; r < UNROLL; ++r) {
-      const int64_t u = base + int64_t(r) * blockDim.x;
-      if (u < units) {
-        a[r] = __builtin_nontemporal_load(dst + u);
-        b[r] = __builtin_nontemporal_load(src + u);
+      for (int r = 0; r < UNROLL; ++r) {
+        const int64_t u = base + int64_t(r) * 256;
+        if (u < a.units) {
+          x[r] = __builtin_nontemporal_load(dst + u);
+          y[r] = __builtin_nontemporal_load(src + u);
+        }
       }
-    }
 #pragma unroll
-    for (int r = 0; r < UNROLL; ++r) {
-      const int64_t u = base + int64_t(r) * blockDim.x;
-      if (u < units) {
-        f32x4 o;
+      for (int r = 0; r < UNROLL; ++r) {
+        const int64_t u = base + int64_t(r) * 256;
+        if (u < a.units) {
+          u32x4 o;
+          if constexpr (BF16) {
 #pragma unroll
-        for (int w = 0; w < 4; ++w) o[w] = float(wa * double(a[r][w]) + wb * double(b[r][w]));
-        __builtin_nontemporal_store(o, dst + u);
+            for (int w = 0; w < 4; ++w) {
+              const double lo = wa * bf16_lo(x[r][w]) + wb * bf16_lo(y[r][w]);
+              const double hi = wa * bf16_hi(x[r][w]) + wb * bf16_hi(y[r][w]);
+              o[w] = pack_bf16_rne(lo, hi);
+            }
+          } else {
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              const double v = wa * double(__uint_as_float(x[r][w])) + wb * double(__uint_as_float(y[r][w]));
+              o[w] = __float_as_uint(float(v));
+            }
+          }
+          __builtin_nontemporal_store(o, dst + u);
+        }
       }
     }
   }
@@ -329,10 +337,12 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
   Layout L{};
   L.slots = cfg->budget + 1;
   size_t off = round_up(sizeof(DevHeader), 256);
-  L.off_first = off;   off = round_up(off + 8 * size_t(L.slots), 256);
-  L.off_pos_sum = off; off = round_up(off + 8 * size_t(L.slots), 256);
-  L.off_span = off;    off = round_up(off + 8 * size_t(L.slots), 256);
-  L.off_order = off;   off = round_up(off + 4 * size_t(L.slots), 256);
+  for (int c = 0; c < 2; ++c) {
+    L.off_first[c] = off;   off = round_up(off + 8 * size_t(L.slots), 256);
+    L.off_pos_sum[c] = off; off = round_up(off + 8 * size_t(L.slots), 256);
+    L.off_span[c] = off;    off = round_up(off + 8 * size_t(L.slots), 256);
+    L.off_order[c] = off;   off = round_up(off + 4 * size_t(L.slots), 256);
+  }
   L.off_log = off;     off = round_up(off + 4 * size_t(kLogCap), 256);
   L.meta_bytes = off;
   L.elt = cfg->dtype == FADEMEM_BF16 ? 2 : 4;
@@ -392,18 +402,16 @@ int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_
   c->pool = static_cast<char*>(dev_pool);
   c->count = 0;
   c->newest = 0;
+  c->inserted = 0;
+  c->cur = 0;
   c->any_inserted = false;
   c->last_hip_error = 0;
   (void)hipGetLastError();
   const unsigned blocks = unsigned((L.slots + 255) / 256);
-  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, as_stream(stream),
-                     reinterpret_cast<DevHeader*>(c->pool), reinterpret_cast<int32_t*>(c->pool + L.off_order),
-                     L.slots);
+  hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, as_stream(stream), c->pool, L);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
-    int err = int(e);
     delete c;
-    (void)err;
     return FADEMEM_EHIP;
   }
   *out = c;
@@ -432,6 +440,11 @@ int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v,
   }
   if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
   if (c->any_inserted && position <= c->newest) return FADEMEM_ESTATE;
+  // t*s_i and first*s_i must stay exact in int64: |t| * (blocks ever held) < 2^62.
+  {
+    const unsigned __int128 mag = (unsigned __int128)(position < 0 ? -position : position) + 1;
+    if (mag * (unsigned __int128)(c->inserted + 1) >= ((unsigned __int128)1 << 62)) return FADEMEM_ESTATE;
+  }
   (void)hipGetLastError();
   const int64_t units = int64_t(c->lay.blk_bytes / 16);
   for (int l0 = 0; l0 < layers; l0 += kMaxLayersPerLaunch) {
@@ -448,6 +461,7 @@ int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v,
     a.units = units;
     a.index = c->count;
     a.position = position;
+    a.cur = c->cur;
     a.write_meta = (l0 == 0);
     hipLaunchKernelGGL(insert_kernel, dim3(plane_blocks(units, 4), unsigned(2 * nl)), dim3(256), 0,
                        as_stream(stream), a);
@@ -455,6 +469,7 @@ int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v,
     if (e != hipSuccess) return hip_fail(c, e);
   }
   c->count += 1;
+  c->inserted += 1;
   c->newest = position;
   c->any_inserted = true;
   return FADEMEM_OK;
@@ -464,22 +479,33 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   if (!c) return FADEMEM_EINVAL;
   if (c->count <= c->cfg.budget) return FADEMEM_OK;  // Alg. S1: within budget, nothing to do
   (void)hipGetLastError();
-  const int n = int(c->count);
-  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(1024), 0, as_stream(stream), c->pool, c->lay, n, c->newest,
-                     c->cfg.beta, c->cfg.anchor);
+  ConsolidateArgs a;
+  a.pool = c->pool;
+  a.lay = c->lay;
+  a.n = int(c->count);
+  a.layers = c->cfg.layers;
+  a.t = c->newest;
+  a.beta = c->cfg.beta;
+  a.anchor = c->cfg.anchor;
+  a.cur = c->cur;
+  a.units = int64_t(c->lay.blk_bytes / 16);
+  // Blocks per plane: enough to cover it with UNROLL units per thread, but
+  // about 2048 blocks in total (8 per CU) so that every block has work and
+  // the per-block schedule evaluation stays a small fraction of the pass.
+  const unsigned planes = unsigned(2 * c->cfg.layers);
+  unsigned per_plane = 2048u / planes;
+  if (per_plane < 1) per_plane = 1;
+  const unsigned cover = plane_blocks(a.units, kMergeUnroll);
+  if (per_plane > cover) per_plane = cover;
+  const dim3 blocks(per_plane, planes);
+  if (c->cfg.dtype == FADEMEM_BF16) {
+    hipLaunchKernelGGL((consolidate_kernel<true, kMergeUnroll>), dim3(blocks), dim3(256), 0, as_stream(stream), a);
+  } else {
+    hipLaunchKernelGGL((consolidate_kernel<false, kMergeUnroll>), dim3(blocks), dim3(256), 0, as_stream(stream), a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(c, e);
-  const int64_t units = int64_t(c->lay.blk_bytes / 16);
-  const dim3 grid(plane_blocks(units, kMergeUnroll), unsigned(2 * c->cfg.layers));
-  if (c->cfg.dtype == FADEMEM_BF16) {
-    hipLaunchKernelGGL(merge_kernel_bf16<kMergeUnroll>, grid, dim3(256), 0, as_stream(stream), c->pool, c->lay,
-                       units);
-  } else {
-    hipLaunchKernelGGL(merge_kernel_f32<kMergeUnroll>, grid, dim3(256), 0, as_stream(stream), c->pool, c->lay,
-                       units);
-  }
-  e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(c, e);
+  c->cur ^= 1;
   c->count -= 1;
   return FADEMEM_OK;
 }
@@ -502,7 +528,7 @@ int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tok
   a.out = out;
   a.lse = lse;
   a.kv_layer_base = c->pool + kv_offset(c->lay, layer, 0, 0);
-  a.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order);
+  a.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order[c->cur]);
   a.k_cur = k_cur;
   a.v_cur = v_cur;
   a.n_entries = c->count;
@@ -529,8 +555,9 @@ int fademem_get_state(fademem_cache* c, int64_t* count, int64_t* first, int64_t*
   const size_t n = size_t(c->count);
   if (count) *count = c->count;
   if (newest) *newest = c->any_inserted ? c->newest : 0;
-  struct Item { int64_t* dst; size_t off; } items[3] = {{first, c->lay.off_first}, {span, c->lay.off_span},
-                                                        {pos_sum, c->lay.off_pos_sum}};
+  struct Item { int64_t* dst; size_t off; } items[3] = {{first, c->lay.off_first[c->cur]},
+                                                        {span, c->lay.off_span[c->cur]},
+                                                        {pos_sum, c->lay.off_pos_sum[c->cur]}};
   for (const Item& it : items) {
     if (it.dst && n > 0) {
       e = hipMemcpy(it.dst, c->pool + it.off, n * sizeof(int64_t), hipMemcpyDeviceToHost);
@@ -546,7 +573,7 @@ int fademem_entry_kv(fademem_cache* c, int32_t layer, int64_t i, const void** k,
   hipError_t e = hipStreamSynchronize(as_stream(stream));
   if (e != hipSuccess) return hip_fail(c, e);
   int32_t slot = 0;
-  e = hipMemcpy(&slot, c->pool + c->lay.off_order + 4 * size_t(i), sizeof(int32_t), hipMemcpyDeviceToHost);
+  e = hipMemcpy(&slot, c->pool + c->lay.off_order[c->cur] + 4 * size_t(i), sizeof(int32_t), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(c, e);
   *k = c->pool + kv_offset(c->lay, layer, slot, 0);
   *v = c->pool + kv_offset(c->lay, layer, slot, 1);

@@ -16,37 +16,33 @@ constexpr int kMaxLayersPerLaunch = 64;   // layer pointers passed as kernel arg
 constexpr int64_t kMaxPosition = int64_t(1) << 40;
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
 
-enum MergeKind : int32_t { kMergeNone = 0, kMergeWeighted = 1, kMergeAnchor = 2 };
-
 // Device-resident header at the start of the pool.  Written only by the
-// library's kernels; the host reads it back for get_state / merge_log.
+// library's kernels; the host reads it back for merge_log.
 struct DevHeader {
   int64_t merges_total;   // consolidations run (length of the merge log)
-  int32_t desc_kind;      // MergeKind of the most recent consolidation
-  int32_t desc_dst_slot;  // slot of entry j (receives the merged block)
-  int32_t desc_src_slot;  // slot of entry j+1 (freed)
-  int32_t pad0;
-  double desc_w_dst;      // w_j
-  double desc_w_src;      // w_{j+1}
+  int64_t anchor_merges;  // of which anchor merges (no K/V work)
 };
 
-// Pool layout.  Metadata arrays are indexed by logical entry (0 = oldest);
-// order[] maps logical entry -> KV slot.  order[] is a permutation of
-// 0..M, its first `count` elements are the live entries' slots and the rest
-// are free slots, so compaction never moves KV.
+// Pool layout.  The memory's metadata is kept twice (copies 0 and 1): a
+// consolidation reads the current copy and writes the other one, so the
+// many blocks of the merge kernel that all derive the schedule decision
+// from the metadata never race with the block that updates it.  Arrays are
+// indexed by logical entry (0 = oldest); order[] maps logical entry -> KV
+// slot and is a permutation of 0..M whose first `count` elements are the
+// live entries' slots (the rest are free), so compaction never moves KV.
 struct Layout {
-  int64_t slots;       // M + 1
-  size_t off_first;    // int64[slots]
-  size_t off_pos_sum;  // int64[slots]
-  size_t off_span;     // int64[slots]
-  size_t off_order;    // int32[slots]
-  size_t off_log;      // int32[kLogCap]
-  size_t meta_bytes;   // multiple of 256
-  size_t elt;          // bytes per element
-  size_t blk_bytes;    // N*H*D*elt: one K (or V) block
-  size_t blk_stride;   // blk_bytes rounded up to 256
-  size_t row_elems;    // H*D: elements per token row
-  size_t total;        // meta_bytes + layers*slots*2*blk_stride
+  int64_t slots;          // M + 1
+  size_t off_first[2];    // int64[slots]
+  size_t off_pos_sum[2];  // int64[slots]
+  size_t off_span[2];     // int64[slots]
+  size_t off_order[2];    // int32[slots]
+  size_t off_log;         // int32[kLogCap]
+  size_t meta_bytes;      // multiple of 256
+  size_t elt;             // bytes per element
+  size_t blk_bytes;       // N*H*D*elt: one K (or V) block
+  size_t blk_stride;      // blk_bytes rounded up to 256
+  size_t row_elems;       // H*D: elements per token row
+  size_t total;           // meta_bytes + layers*slots*2*blk_stride
 };
 
 int compute_layout(const fademem_config* cfg, Layout* lay);
