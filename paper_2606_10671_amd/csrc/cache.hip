@@ -351,7 +351,9 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
   if (blk > 1e15) return FADEMEM_EINVAL;
   L.blk_bytes = size_t(cfg->tokens_per_block) * L.row_elems * L.elt;
   L.blk_stride = round_up(L.blk_bytes, 256);
-  L.total = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
+  L.off_ws = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
+  L.ws_bytes = cfg->dtype == FADEMEM_BF16 ? attend_ws_bytes(cfg->head_dim) : 0;
+  L.total = L.off_ws + L.ws_bytes;
   *lay = L;
   return FADEMEM_OK;
 }
@@ -537,6 +539,7 @@ int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tok
   a.q_tokens = q_tokens;
   a.slot_stride = 2 * c->lay.blk_stride;
   a.v_offset = c->lay.blk_stride;
+  a.ws = reinterpret_cast<float*>(c->pool + c->lay.off_ws);
   a.heads = c->cfg.heads;
   a.head_dim = c->cfg.head_dim;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf(float(c->cfg.head_dim));

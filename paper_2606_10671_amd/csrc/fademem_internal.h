@@ -16,6 +16,21 @@ constexpr int kMaxLayersPerLaunch = 64;   // layer pointers passed as kernel arg
 constexpr int64_t kMaxPosition = int64_t(1) << 40;
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
 
+// bf16 attention work split.  The key range of every query tile is cut into
+// equal shares for at most kSkMaxGroups resident workgroups; a share that
+// covers part of a query tile leaves a partial result (unnormalised O, row
+// max and row sums) in one of two scratch slots per workgroup, and a second
+// kernel merges the partials of each split tile.
+constexpr int kAttnThreads = 256;        // threads per workgroup (4 waves)
+constexpr int kAttnQueries = 128;        // queries per workgroup (32 per wave)
+constexpr int kSkMaxGroups = 512;        // workgroups of one launch at most
+__host__ __device__ constexpr size_t attend_slot_floats(int head_dim) {
+  return size_t(kAttnQueries) * size_t(head_dim) + 2 * size_t(kAttnThreads);
+}
+__host__ __device__ constexpr size_t attend_ws_bytes(int head_dim) {
+  return 2 * size_t(kSkMaxGroups) * attend_slot_floats(head_dim) * sizeof(float);
+}
+
 // Device-resident header at the start of the pool.  Written only by the
 // library's kernels; the host reads it back for merge_log.
 struct DevHeader {
@@ -42,7 +57,9 @@ struct Layout {
   size_t blk_bytes;       // N*H*D*elt: one K (or V) block
   size_t blk_stride;      // blk_bytes rounded up to 256
   size_t row_elems;       // H*D: elements per token row
-  size_t total;           // meta_bytes + layers*slots*2*blk_stride
+  size_t off_ws;          // attention scratch (bf16 caches), after the KV region
+  size_t ws_bytes;        // attend_ws_bytes(D) for bf16, 0 for fp32
+  size_t total;           // off_ws + ws_bytes
 };
 
 int compute_layout(const fademem_config* cfg, Layout* lay);
@@ -70,6 +87,7 @@ struct AttendArgs {
   int64_t q_tokens;
   size_t slot_stride;         // bytes between consecutive slots' K blocks (2*blk_stride)
   size_t v_offset;            // bytes from a slot's K block to its V block
+  float* ws;                  // attention scratch (bf16): 2*kSkMaxGroups slots
   int heads;
   int head_dim;
   float scale;

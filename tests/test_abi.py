@@ -47,13 +47,19 @@ GOOD = dict(budget=21, heads=12, head_dim=128, tokens_per_block=1560, beta=0.3, 
 
 
 def test_pool_bytes_layout():
+    """Metadata (< 64 KiB) + (M+1) K and V slots per layer; bf16 caches add
+    the attention's split-work scratch: two slots per workgroup (at most
+    512) of 128 queries x D fp32 partial O plus 256 fp32 maxima and sums."""
     n = fm.fademem_pool_bytes(fm.make_config(**GOOD))
     blk = 1560 * 12 * 128 * 2
-    assert n >= 22 * 2 * blk and n < 22 * 2 * blk + 64 * 1024
+    ws = 2 * 512 * (128 * 128 + 2 * 256) * 4
+    assert n >= 22 * 2 * blk + ws and n < 22 * 2 * blk + ws + 64 * 1024
     n30 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "layers": 30}))
     assert n30 - n == 29 * 22 * 2 * blk
     nf = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "dtype": fm.FADEMEM_F32}))
-    assert nf - n == 22 * 2 * blk
+    assert nf - n == 22 * 2 * blk - ws
+    n64 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "head_dim": 64}))
+    assert n - n64 == 22 * blk + ws - 2 * 512 * (128 * 64 + 2 * 256) * 4
 
 
 @pytest.mark.parametrize("field,value", [("budget", 1), ("budget", 1024), ("heads", 0), ("head_dim", 96),
