@@ -33,6 +33,26 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 FP32_VECTOR_PEAK_TFLOPS = 157.3
 
+# HBM bytes of one steady-state bf16 attention call (main kernel + merge of
+# split tiles) at the wan1.3b-1layer workload, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE (see profiles/attend_bf16_wan1.3b_1layer.md), valid only for the
+# kernel source they were taken on (first 16 hex digits of its sha256).
+ATTN_TRAFFIC = {"source_sha256": "d3dfa5c9801af59a", "workload": "wan1.3b-1layer", "bytes_per_call": 806198415}
+
+
+def attn_traffic(workload):
+    """Measured HBM bytes per attention call, or None if the kernel source
+    changed since the counters were taken or the workload differs."""
+    import hashlib
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_10671_amd", "csrc", "attend_bf16.hip")
+    try:
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    if sha != ATTN_TRAFFIC["source_sha256"] or workload != ATTN_TRAFFIC["workload"]:
+        return None
+    return ATTN_TRAFFIC["bytes_per_call"]
+
 
 def parse():
     p = argparse.ArgumentParser()
@@ -216,12 +236,14 @@ def main():
         "final_spans": state["span"],
         "roofline": {
             "bound": "mfma" if is_bf16 else "alu",
-            "kernel": "attend_bf16_kernel<128>" if is_bf16 else "attend_f32_kernel",
+            "kernel": ("attend_bf16_d128 + attend_bf16_merge_d128 (one attend call)" if D == 128 else
+                       "attend_bf16_d64 + attend_bf16_merge_d64 (one attend call)") if is_bf16 else "attend_f32_kernel",
             "achieved": round(attn_tflops, 2),
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / peak, 4),
-            "traffic": None,
+            "traffic": attn_traffic(args.workload) if is_bf16 else None,
+            "traffic_unit": "bytes per call (HBM read + write)",
         },
     }
     if not args.no_cpu_baseline:
