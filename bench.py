@@ -62,13 +62,15 @@ def parse():
     p.add_argument("--workload", default="wan1.3b-1layer", choices=sorted(WORKLOADS))
     p.add_argument("--beta", type=float, default=0.3)
     p.add_argument("--no-anchor", action="store_true")
+    p.add_argument("--merge-op", default="sqrt_span", choices=["sqrt_span", "average", "select_nearest", "max"],
+                   help="consolidation operator (Sec. 3.3 default, or a Table 4 ablation)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
 
-def cpu_baseline(wl, head_inputs, beta, anchor, budget_s):
+def cpu_baseline(wl, head_inputs, beta, anchor, budget_s, merge_op="sqrt_span"):
     """The oracle, as it stands, on the host cores: one steady-state chunk
     step (memory full, F merges), restricted to whole heads, as many heads
     as fit the time budget, scaled to all heads and layers (the step is
@@ -80,7 +82,7 @@ def cpu_baseline(wl, head_inputs, beta, anchor, budget_s):
     heads_done, t_total = 0, 0.0
     for h in range(H):
         q, k, v, fill_k, fill_v = head_inputs(h)
-        oc = OracleCache(budget=wl["budget"], beta=beta, anchor=anchor, storage=wl["dtype"])
+        oc = OracleCache(budget=wl["budget"], beta=beta, anchor=anchor, storage=wl["dtype"], operator=merge_op)
         for t in range(len(fill_k)):          # fill the memory (untimed)
             oc.update(fill_k[t], fill_v[t], t)
         t0 = time.perf_counter()
@@ -135,7 +137,7 @@ def main():
         inputs.append(per_layer)
     out = torch.empty((F * N, H, D), dtype=tdtype, device=dev)
     cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=args.beta, anchor=anchor,
-                  dtype=tdtype, layers=L, device=dev)
+                  dtype=tdtype, layers=L, device=dev, merge_op=args.merge_op)
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -199,9 +201,11 @@ def main():
     attn_flop = 4.0 * (F * N) * lk * D * H  # QK^T and PV, per layer-call
     attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
     attn_tflops = attn_flop / attn_avg_s / 1e12
-    merge_bytes = weighted * 3 * 2 * blk * L
+    # A weighted (or averaged, or max-pooled) merge reads two entries' K and V
+    # and writes one; Select Nearest re-points a slot and moves no bytes.
+    merge_bytes = 0 if args.merge_op == "select_nearest" else weighted * 3 * 2 * blk * L
     cons_s = sum(cons_ms) / 1e3
-    merge_gbps = merge_bytes / cons_s / 1e9 if cons_s > 0 else None
+    merge_gbps = merge_bytes / cons_s / 1e9 if cons_s > 0 and merge_bytes > 0 else None
     ins_gbps = len(ins_ms) * 2 * 2 * blk * L / (sum(ins_ms) / 1e3) / 1e9
 
     state = cache_timed.state()
@@ -223,7 +227,8 @@ def main():
         "data": "synthetic: seeded AR(1) K/V stream (rho 0.95, noise 0.5), N(0,1) Q, device-generated",
         "config": {"workload": args.workload, "heads": H, "head_dim": D, "tokens_per_block": N,
                    "frames_per_chunk": F, "query_tokens": F * N, "budget": M, "beta": args.beta,
-                   "anchor": anchor, "layers": L, "chunks": chunks, "keys_per_attend": lk},
+                   "anchor": anchor, "merge_op": args.merge_op, "layers": L, "chunks": chunks,
+                   "keys_per_attend": lk},
         "attention_tflops": round(attn_tflops, 2),
         "attention_ms_per_call": round(attn_avg_s * 1e3, 4),
         "merge_gbps": round(merge_gbps, 1) if merge_gbps else None,
@@ -261,7 +266,7 @@ def main():
                     fill_k.append(host(kc[f * N:(f + 1) * N]))
                     fill_v.append(host(vc[f * N:(f + 1) * N]))
             return host(q), host(k), host(v), fill_k, fill_v
-        result["cpu_baseline"] = cpu_baseline(wl, head_inputs, args.beta, anchor, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(wl, head_inputs, args.beta, anchor, args.cpu_seconds, args.merge_op)
     print(json.dumps(result), flush=True)
 
 

@@ -53,9 +53,24 @@ enum {
 
 enum { FADEMEM_F32 = 0, FADEMEM_BF16 = 1 };
 
-/* Consolidation operators (Sec. 3.3 "Consolidation operator"; Table 4).
- * Only the paper's default is implemented in this build. */
-enum { FADEMEM_MERGE_SQRT_SPAN = 0 };
+/* Consolidation operators: the K, V rule of a merge (Sec. 3.3
+ * "Consolidation operator"; the ablation of Sec. 4.3, Table 4).  The
+ * metadata rule (spans add, mu span-weighted) and the anchor's branch are
+ * the same for all.
+ *   SQRT_SPAN      X = (sqrt(s_j) X_j + sqrt(s_j+1) X_j+1) / (sqrt(s_j) + sqrt(s_j+1)),
+ *                  the paper's default, in fp64, one RNE rounding to the storage type;
+ *   AVERAGE        the same with both weights 1/2 (unweighted average);
+ *   SELECT_NEAREST the newer entry's K, V (representative selection; no
+ *                  K/V bytes move: the merged entry takes the newer one's slot);
+ *   MAX            elementwise max pooling; the newer value wins only when
+ *                  strictly greater (equal values, -0 and +0 included, keep
+ *                  the older entry's bits). */
+enum {
+  FADEMEM_MERGE_SQRT_SPAN = 0,
+  FADEMEM_MERGE_AVERAGE = 1,
+  FADEMEM_MERGE_SELECT_NEAREST = 2,
+  FADEMEM_MERGE_MAX = 3
+};
 
 typedef struct fademem_config {
   int64_t budget;           /* M, the entry budget (Sec. 3.1); 2 <= M <= 1023.
@@ -69,7 +84,7 @@ typedef struct fademem_config {
                                (Sec. 3.3); the paper's default is 0.3 (Sec. 4.1) */
   int32_t anchor;           /* 1: the first inserted block is a global anchor
                                (Sec. 3.3, Alg. S1), the paper's default; 0: off */
-  int32_t merge_op;         /* FADEMEM_MERGE_SQRT_SPAN                          */
+  int32_t merge_op;         /* FADEMEM_MERGE_* (default SQRT_SPAN)              */
   int32_t dtype;            /* FADEMEM_F32 or FADEMEM_BF16 for K, V, Q, O      */
   int32_t layers;           /* L >= 1 per-layer memories sharing one schedule.
                                The schedule depends only on positions, so every
@@ -87,7 +102,7 @@ int fademem_pool_bytes(const fademem_config* cfg, size_t* bytes);
  * `stream` (the pool's previous contents do not matter).  The memory starts
  * empty.  *out receives a host handle to destroy with fademem_cache_destroy.
  * Errors: EINVAL (config, NULL or misaligned pool), ENOMEM (pool too small),
- * EUNSUPPORTED (merge_op), EHIP. */
+ * EHIP. */
 int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_bytes,
                          void* stream, fademem_cache** out);
 
@@ -112,10 +127,11 @@ int fademem_insert(fademem_cache* cache, const void* const* k, const void* const
  * adjacent pairs except the one holding the newest entry, j = the smallest
  * gap (gaps within a relative 1e-9 of the smallest count as tied and the
  * oldest such pair wins); the pair is replaced by its consolidation: spans
- * add, mu is span-weighted; K, V = sqrt-span weighted average evaluated in
- * fp64 and rounded once (round-to-nearest-even) to the storage type; when
- * the pair holds the anchor its K, V and position are kept (Sec. 3.3,
- * Alg. S1).  The decision never crosses to the host.  Errors: EHIP. */
+ * add, mu is span-weighted; K, V by the configured operator (default:
+ * sqrt-span weighted average evaluated in fp64 and rounded once,
+ * round-to-nearest-even, to the storage type); when the pair holds the
+ * anchor its K, V and position are kept (Sec. 3.3, Alg. S1).  The decision
+ * never crosses to the host.  Errors: EHIP. */
 int fademem_consolidate(fademem_cache* cache, void* stream);
 
 /* Attention of the chunk's queries over layer `layer`'s exposed cache:

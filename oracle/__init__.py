@@ -6,6 +6,7 @@ this package.  The product library never does.
 from .fademem_oracle import (  # noqa: F401
     Entry,
     OracleCache,
+    OPERATORS,
     TIE_RTOL,
     attend,
     bf16_bits,

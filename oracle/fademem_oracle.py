@@ -17,7 +17,10 @@ What it computes (FadeMem, arXiv 2606.10671):
 * Consolidation operator -- Sec. 3.3 "Consolidation operator": spans add,
   mu is the span-weighted mean, K and V are square-root-span weighted
   averages.  The first-frame anchor keeps its K, V and position when its
-  pair is chosen (Algorithm S1, supplementary Sec. S1).
+  pair is chosen (Algorithm S1, supplementary Sec. S1).  The ablation of
+  Sec. 4.3 ("Memory consolidation operator", Table 4) swaps the K, V rule
+  for an unweighted average, a representative selection ("Select Nearest")
+  or elementwise max pooling; the metadata rule is the same for all.
 * Attention -- Sec. 3.1: the chunk's queries attend over the exposed cache
   [memory entries in order || current chunk].  This is textbook softmax
   attention, written out in fp64.
@@ -36,7 +39,11 @@ design notes of the repository):
   (two products and one sum, each rounded to fp64) and rounded once to the
   storage type (fp32, or bf16 with round-to-nearest-even);
 * a chunk of F frames runs F insert+consolidate updates in frame order,
-  after the chunk's attention call.
+  after the chunk's attention call;
+* "Select Nearest" keeps the newer entry's K, V (the entry nearer to the
+  present, whose distance the schedule measures); max pooling takes, per
+  element, the newer entry's value when it is strictly greater, else the
+  older one's (so equal values, including -0 and +0, keep the older bits).
 
 Parity status: every function here is pinned by tests under tests/ (see
 tests/test_oracle_*.py) except where a docstring says "parity unpinned".
@@ -51,6 +58,7 @@ from typing import List, Optional, Sequence, Tuple
 import numpy as np
 
 TIE_RTOL = 1e-9  # relative tolerance under which two gaps count as tied
+OPERATORS = ("sqrt_span", "average", "select_nearest", "max")  # Sec. 3.3 default, then Table 4
 
 
 # ---------------------------------------------------------------------------
@@ -130,11 +138,15 @@ class OracleCache:
     beta    -- exponent of u(d) = d**beta, 0 < beta <= 1 (Sec. 3.3).
     anchor  -- keep the first block as a global anchor (Sec. 3.3, S1).
     storage -- "f32" or "bf16": the type merged K, V are stored in.
+    operator -- the K, V rule of a merge: "sqrt_span" (the default of
+               Sec. 3.3), or one of the Table 4 ablations "average",
+               "select_nearest", "max".
     """
     budget: int
     beta: float = 0.3
     anchor: bool = True
     storage: str = "f32"
+    operator: str = "sqrt_span"
     entries: List[Entry] = field(default_factory=list)
     newest: Optional[int] = None
     merge_log: List[int] = field(default_factory=list)
@@ -148,6 +160,8 @@ class OracleCache:
             raise ValueError("beta must satisfy 0 < beta <= 1")
         if self.storage not in ("f32", "bf16"):
             raise ValueError("storage must be 'f32' or 'bf16'")
+        if self.operator not in OPERATORS:
+            raise ValueError(f"operator must be one of {OPERATORS}")
 
     # -- storage rounding -------------------------------------------------
     def _store(self, x64: np.ndarray) -> np.ndarray:
@@ -218,9 +232,23 @@ class OracleCache:
         return w_j, 1.0 - w_j
 
     def merge_values(self, a: Entry, b: Entry) -> Tuple[np.ndarray, np.ndarray]:
-        """K_new = w_j K_j + w_{j+1} K_{j+1} (and V likewise) in fp64, then
-        one rounding to the storage type."""
-        w_j, w_j1 = self.weights(a.span, b.span)
+        """K, V of the merged entry under the configured operator:
+
+        sqrt_span      -- K_new = w_j K_j + w_{j+1} K_{j+1} with the weights
+                          above (Sec. 3.3), in fp64, then one rounding to the
+                          storage type;
+        average        -- the same with w_j = w_{j+1} = 1/2 (Table 4);
+        select_nearest -- the newer entry's K, V as stored (Table 4);
+        max            -- elementwise maximum of the stored values (Table 4).
+        """
+        if self.operator == "select_nearest":
+            return b.K.copy(), b.V.copy()
+        if self.operator == "max":
+            return tuple(np.where(xb > xa, xb, xa) for xa, xb in ((a.K, b.K), (a.V, b.V)))
+        if self.operator == "average":
+            w_j, w_j1 = 0.5, 0.5
+        else:
+            w_j, w_j1 = self.weights(a.span, b.span)
         out = []
         for xa, xb in ((a.K, b.K), (a.V, b.V)):
             xa64 = xa.astype(np.float64)

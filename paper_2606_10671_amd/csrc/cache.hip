@@ -166,6 +166,7 @@ struct ConsolidateArgs {
   double beta;
   int anchor;
   int cur;          // metadata copy read; the other copy is written
+  int op;           // FADEMEM_MERGE_*
   int64_t units;    // 16-byte units per K (or V) block
 };
 
@@ -185,7 +186,7 @@ struct ConsolidateArgs {
 // products and one sum, rounded once to the storage type.  The blocks of
 // each (layer, K|V) plane stride over it with 16-byte nontemporal
 // loads/stores, UNROLL units in flight per thread; grid.y = layer * 2 + kv.
-template <bool BF16, int UNROLL>
+template <bool BF16, int UNROLL, bool MAXOP>
 __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
 #pragma clang fp contract(off)
   __shared__ double u_s[kMaxBudget + 1];
@@ -220,6 +221,11 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
   const bool anchor_pair = a.anchor && j == 0;
   const int32_t dst_slot = m.order[j];
   const int32_t src_slot = m.order[j + 1];
+  // Select Nearest keeps the newer entry's K, V: the merged entry takes its
+  // slot and the older entry's slot is freed (no K/V bytes move).
+  const bool select = a.op == FADEMEM_MERGE_SELECT_NEAREST && !anchor_pair;
+  const int32_t keep_slot = select ? src_slot : dst_slot;
+  const int32_t free_slot = select ? dst_slot : src_slot;
 
   if (blockIdx.x == 0 && blockIdx.y == 0) {
     const Meta w = meta_of(a.pool, a.lay, a.cur ^ 1);
@@ -234,14 +240,14 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
         w.first[i] = m.first[j];
         w.pos_sum[i] = anchor_pair ? m.first[j] * s_new : m.pos_sum[j] + m.pos_sum[j + 1];
         w.span[i] = s_new;
-        w.order[i] = dst_slot;
+        w.order[i] = keep_slot;
       } else if (i < n - 1) {
         w.first[i] = m.first[i + 1];
         w.pos_sum[i] = m.pos_sum[i + 1];
         w.span[i] = m.span[i + 1];
         w.order[i] = m.order[i + 1];
       } else {
-        w.order[i] = src_slot;  // freed slot
+        w.order[i] = free_slot;
       }
     }
     // order[] keeps all M+1 slots: copy the free tail beyond the held entries.
@@ -255,11 +261,11 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
       if (anchor_pair) hdr->anchor_merges += 1;
     }
   }
-  if (anchor_pair) return;  // the anchor keeps its K and V; nothing to move
+  if (anchor_pair || select) return;  // the anchor keeps its K and V; selection moves nothing
 
   const double rj = sqrt(double(s_j));
   const double rj1 = sqrt(double(s_j1));
-  const double wa = rj / (rj + rj1);
+  const double wa = a.op == FADEMEM_MERGE_AVERAGE ? 0.5 : rj / (rj + rj1);
   const double wb = 1.0 - wa;
   const int64_t step = int64_t(gridDim.x) * 256 * UNROLL;
   {
@@ -282,7 +288,22 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
         const int64_t u = base + int64_t(r) * 256;
         if (u < a.units) {
           u32x4 o;
-          if constexpr (BF16) {
+          if constexpr (MAXOP) {
+            // Max pooling: the newer value (y) only when strictly greater,
+            // so equal values keep the older bits.
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+              if constexpr (BF16) {
+                const uint32_t xl = x[r][w] << 16, yl = y[r][w] << 16;
+                const uint32_t xh = x[r][w] & 0xFFFF0000u, yh = y[r][w] & 0xFFFF0000u;
+                const uint32_t lo = (__uint_as_float(yl) > __uint_as_float(xl)) ? yl : xl;
+                const uint32_t hi = (__uint_as_float(yh) > __uint_as_float(xh)) ? yh : xh;
+                o[w] = (lo >> 16) | hi;
+              } else {
+                o[w] = (__uint_as_float(y[r][w]) > __uint_as_float(x[r][w])) ? y[r][w] : x[r][w];
+              }
+            }
+          } else if constexpr (BF16) {
 #pragma unroll
             for (int w = 0; w < 4; ++w) {
               const double lo = wa * bf16_lo(x[r][w]) + wb * bf16_lo(y[r][w]);
@@ -324,6 +345,7 @@ bool valid_config(const fademem_config* c) {
   if (!(c->beta > 0.0 && c->beta <= 1.0)) return false;
   if (c->anchor != 0 && c->anchor != 1) return false;
   if (c->dtype != FADEMEM_F32 && c->dtype != FADEMEM_BF16) return false;
+  if (c->merge_op < FADEMEM_MERGE_SQRT_SPAN || c->merge_op > FADEMEM_MERGE_MAX) return false;
   if (c->layers < 1 || c->layers > 4096) return false;
   return true;
 }
@@ -394,7 +416,6 @@ int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_
   Layout L;
   int rc = compute_layout(cfg, &L);
   if (rc) return rc;
-  if (cfg->merge_op != FADEMEM_MERGE_SQRT_SPAN) return FADEMEM_EUNSUPPORTED;
   if (!dev_pool || !aligned(dev_pool, 256)) return FADEMEM_EINVAL;
   if (pool_bytes < L.total) return FADEMEM_ENOMEM;
   fademem_cache* c = new (std::nothrow) fademem_cache();
@@ -489,6 +510,7 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   a.t = c->newest;
   a.beta = c->cfg.beta;
   a.anchor = c->cfg.anchor;
+  a.op = c->cfg.merge_op;
   a.cur = c->cur;
   a.units = int64_t(c->lay.blk_bytes / 16);
   // Blocks per plane: enough to cover it with UNROLL units per thread, but
@@ -500,11 +522,10 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   const unsigned cover = plane_blocks(a.units, kMergeUnroll);
   if (per_plane > cover) per_plane = cover;
   const dim3 blocks(per_plane, planes);
-  if (c->cfg.dtype == FADEMEM_BF16) {
-    hipLaunchKernelGGL((consolidate_kernel<true, kMergeUnroll>), dim3(blocks), dim3(256), 0, as_stream(stream), a);
-  } else {
-    hipLaunchKernelGGL((consolidate_kernel<false, kMergeUnroll>), dim3(blocks), dim3(256), 0, as_stream(stream), a);
-  }
+  const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
+  auto kernel = bf16 ? (maxop ? consolidate_kernel<true, kMergeUnroll, true> : consolidate_kernel<true, kMergeUnroll, false>)
+                     : (maxop ? consolidate_kernel<false, kMergeUnroll, true> : consolidate_kernel<false, kMergeUnroll, false>);
+  hipLaunchKernelGGL(kernel, dim3(blocks), dim3(256), 0, as_stream(stream), a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(c, e);
   c->cur ^= 1;

@@ -23,6 +23,11 @@ FADEMEM_EUNSUPPORTED = -5
 FADEMEM_F32 = 0
 FADEMEM_BF16 = 1
 FADEMEM_MERGE_SQRT_SPAN = 0
+FADEMEM_MERGE_AVERAGE = 1
+FADEMEM_MERGE_SELECT_NEAREST = 2
+FADEMEM_MERGE_MAX = 3
+MERGE_OPS = {"sqrt_span": FADEMEM_MERGE_SQRT_SPAN, "average": FADEMEM_MERGE_AVERAGE,
+             "select_nearest": FADEMEM_MERGE_SELECT_NEAREST, "max": FADEMEM_MERGE_MAX}
 
 EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
@@ -205,14 +210,17 @@ class Cache:
     """
 
     def __init__(self, budget: int, heads: int, head_dim: int, tokens_per_block: int, beta: float = 0.3,
-                 anchor: bool = True, dtype=None, layers: int = 1, device=None):
+                 anchor: bool = True, dtype=None, layers: int = 1, device=None, merge_op: str = "sqrt_span"):
         import torch
         dtype = torch.bfloat16 if dtype is None else dtype
         if dtype not in (torch.float32, torch.bfloat16):
             raise ValueError("dtype must be torch.float32 or torch.bfloat16")
+        if merge_op not in MERGE_OPS:
+            raise ValueError(f"merge_op must be one of {sorted(MERGE_OPS)}")
         self.torch_dtype = dtype
         self.cfg = make_config(budget, heads, head_dim, tokens_per_block, beta, anchor,
-                               FADEMEM_BF16 if dtype == torch.bfloat16 else FADEMEM_F32, layers)
+                               FADEMEM_BF16 if dtype == torch.bfloat16 else FADEMEM_F32, layers,
+                               merge_op=MERGE_OPS[merge_op])
         self.device = torch.device("cuda") if device is None else torch.device(device)
         self.pool_bytes = fademem_pool_bytes(self.cfg)
         self.pool = torch.empty(self.pool_bytes, dtype=torch.uint8, device=self.device)

@@ -64,7 +64,8 @@ def test_pool_bytes_layout():
 
 @pytest.mark.parametrize("field,value", [("budget", 1), ("budget", 1024), ("heads", 0), ("head_dim", 96),
                                          ("tokens_per_block", 0), ("beta", 0.0), ("beta", 1.0001),
-                                         ("beta", float("nan")), ("anchor", 2), ("dtype", 7), ("layers", 0)])
+                                         ("beta", float("nan")), ("anchor", 2), ("dtype", 7), ("layers", 0),
+                                         ("merge_op", -1), ("merge_op", 4)])
 def test_bad_configs_are_rejected(field, value):
     cfg = fm.make_config(**GOOD)
     setattr(cfg, field, value)
@@ -83,9 +84,9 @@ def test_create_validates_before_touching_the_device():
                                   ctypes.byref(h)) == fm.FADEMEM_EINVAL           # misaligned
     assert L.fademem_cache_create(ctypes.byref(cfg), ctypes.c_void_p(4096), need - 1, None,
                                   ctypes.byref(h)) == fm.FADEMEM_ENOMEM
-    cfg.merge_op = 3
+    cfg.merge_op = 4          # no such consolidation operator
     assert L.fademem_cache_create(ctypes.byref(cfg), ctypes.c_void_p(4096), need, None,
-                                  ctypes.byref(h)) == fm.FADEMEM_EUNSUPPORTED
+                                  ctypes.byref(h)) == fm.FADEMEM_EINVAL
     assert h.value is None
     assert L.fademem_cache_create(ctypes.byref(cfg), ctypes.c_void_p(4096), need, None, None) == fm.FADEMEM_EINVAL
 

@@ -161,3 +161,80 @@ def test_anchor_pair_keeps_anchor_bits_and_drops_neighbour():
     assert (a.first, a.span, a.pos_sum) == (10, 2, 20)
     assert np.array_equal(a.K, blocks[0]) and np.array_equal(a.V, vals[0])
     assert np.array_equal(c.entries[1].K, blocks[2])
+
+
+# -- Table 4 operators (Sec. 4.3 "Memory consolidation operator") -------------
+
+def merge_op(operator, storage, sa, sb, Ka, Kb, Va=None, Vb=None):
+    c = OracleCache(budget=4, beta=0.3, storage=storage, operator=operator)
+    a = Entry(0, 0, sa, False, Ka, Ka.copy() if Va is None else Va)
+    b = Entry(sa, sa, sb, False, Kb, Kb.copy() if Vb is None else Vb)
+    return c.merge_values(a, b)
+
+
+def test_unknown_operator_is_rejected():
+    with pytest.raises(ValueError):
+        OracleCache(budget=4, operator="median")
+
+
+@pytest.mark.parametrize("storage", ["f32", "bf16"])
+def test_average_ignores_spans_and_gives_the_nearest_midpoint(storage):
+    """Unweighted average: spans (1, 4) on (0, 3) give 1.5 (the sqrt-span
+    default gives 2), and in general the storage number nearest the exact
+    midpoint (exact fractions; ties to the even pattern)."""
+    z = np.zeros(3, np.float32)
+    K, _ = merge_op("average", storage, 1, 4, z, z + 3)
+    assert np.all(K == 1.5)
+    rng = np.random.default_rng(12)
+    a, b = rng.standard_normal(400) * 5, rng.standard_normal(400) * 5
+    a, b = (round_to_bf16(a), round_to_bf16(b)) if storage == "bf16" else (a.astype(np.float32), b.astype(np.float32))
+    r, _ = merge_op("average", storage, 7, 100, a, b)
+    for x, y, z_ in zip(a, b, r):
+        mid = (Fraction(float(x)) + Fraction(float(y))) / 2
+        if storage == "bf16":
+            bz = int(bf16_bits(np.float32([z_]))[0])
+            nb = [float(bf16_from_bits(np.uint16([(bz + d) & 0xFFFF]))[0]) for d in (-1, 1)]
+        else:
+            nb = [float(np.nextafter(z_, np.float32(-np.inf))), float(np.nextafter(z_, np.float32(np.inf)))]
+        err = abs(Fraction(float(z_)) - mid)
+        assert all(err <= abs(Fraction(n) - mid) for n in nb if np.isfinite(n))
+
+
+def test_select_nearest_keeps_the_newer_bits():
+    rng = np.random.default_rng(13)
+    Ka, Kb = round_to_bf16(rng.standard_normal((4, 3))), round_to_bf16(rng.standard_normal((4, 3)))
+    Va, Vb = round_to_bf16(rng.standard_normal((4, 3))), round_to_bf16(rng.standard_normal((4, 3)))
+    K, V = merge_op("select_nearest", "bf16", 3, 9, Ka, Kb, Va, Vb)
+    assert np.array_equal(K.view(np.uint32), Kb.view(np.uint32))
+    assert np.array_equal(V.view(np.uint32), Vb.view(np.uint32))
+
+
+def test_max_pooling_elementwise_and_signed_zero():
+    """Elementwise maximum (brute force per element); equal values keep the
+    older entry's bits, so max(-0, +0) is -0 when -0 is older."""
+    rng = np.random.default_rng(14)
+    Ka = round_to_bf16(rng.standard_normal(300))
+    Kb = round_to_bf16(rng.standard_normal(300))
+    Ka[:3] = [-0.0, 0.0, 1.0]
+    Kb[:3] = [0.0, -0.0, 1.0]
+    K, _ = merge_op("max", "bf16", 1, 1, Ka, Kb)
+    for i in range(300):
+        want = Kb[i] if float(Kb[i]) > float(Ka[i]) else Ka[i]
+        assert np.float32(K[i]).view(np.uint32) == np.float32(want).view(np.uint32), i
+    assert np.signbit(K[0]) and not np.signbit(K[1])
+
+
+@pytest.mark.parametrize("operator", ["average", "select_nearest", "max"])
+def test_operator_changes_values_not_the_schedule(operator):
+    """The schedule depends only on positions (Sec. 3.3): every operator makes
+    the same decisions and keeps the same metadata as the default, and the
+    anchor still keeps its own K, V bits."""
+    rng = np.random.default_rng(15)
+    ref = OracleCache(budget=5, beta=0.3, anchor=True, storage="bf16")
+    alt = OracleCache(budget=5, beta=0.3, anchor=True, storage="bf16", operator=operator)
+    blocks = [round_to_bf16(rng.standard_normal((3, 2))) for _ in range(30)]
+    for t, blk in enumerate(blocks):
+        ref.update(blk, blk, t)
+        alt.update(blk, blk, t)
+    assert ref.merge_log == alt.merge_log and ref.state() == alt.state()
+    assert np.array_equal(alt.entries[0].K, blocks[0])
