@@ -5,38 +5,43 @@
 // [memory entries in memory order || current chunk] (FadeMem Sec. 3.1 and
 // Sec. 4.1: the chunk attends over the memory entries plus its own frames).
 //
-// Design (workgroup = 4 waves = 128 queries of one head; two workgroups per
-// CU, i.e. two waves per SIMD, so one wave's softmax overlaps the other's
-// MFMAs):
-// * Work split: the (query tile, key tile) iterations of all heads are cut
-//   into equal contiguous shares, one per resident workgroup (stream-K).
-//   A share may end or start inside a query tile; that part's unnormalised
-//   O, running max and partial sums go to a scratch slot, and a second
-//   kernel merges the parts of each split tile.  Every SIMD then carries
-//   the same work, where whole 128-query tiles would leave part of the chip
-//   idle in the last round (e.g. 444 tiles on 512 workgroup slots).
-// * Transposed scores: a wave computes S^T = K Q^T for its 32 queries, so an
-//   accumulator lane holds 16 keys of ONE query.  Row max and sum need one
-//   lane-pair exchange (permlane32 swap) per tile, and P leaves the
-//   accumulator already in the B-operand layout of O^T = V^T P^T.
-// * K/V tiles (64 keys) go from global memory straight into LDS
-//   (global_load_lds, 16 bytes per lane), double-buffered: the next tile's
-//   loads fly during the current tile's math; one barrier per tile.
+// Design (workgroup = 8 waves x 32 queries of one head, one workgroup per
+// CU, two waves per SIMD; every value stays in the 256 architectural VGPRs
+// of a wave):
+// * The 256 queries of a workgroup share each K/V tile, which is streamed
+//   from L2 into LDS once for all of them.
+// * Transposed scores: S^T = K Q^T puts 16 keys of ONE query in each
+//   accumulator lane.  Row max and sum need one lane-pair exchange
+//   (permlane32 swap) per tile, and P leaves the accumulator already in the
+//   B-operand layout of O^T = V^T P^T.
+// * Software pipeline over key tiles of 64: iteration t runs block A =
+//   [S(t+1) = K(t+1) Q^T] beside the exponentials of S(t)'s second 32 keys,
+//   then block B = [O += V(t) P(t)] beside the row max of S(t+1) and the
+//   exponentials of its first 32 keys.  Each block is cut into fenced steps
+//   of four MFMAs that carry their share of the softmax VALU work, the LDS
+//   reads of the next step and one tile load, so one wave always has MFMAs
+//   and independent VALU work in flight.
+// * K/V tiles go from global memory straight into LDS (global_load_lds,
+//   16 bytes per lane), issued two tiles ahead into three-deep rings (each
+//   buffer its own LDS object, so the compiler can tell the reads of one
+//   buffer from the loads in flight into another); one barrier per tile.
 // * K is read with 16-byte LDS loads; V stays row-major in LDS and its V^T
 //   operand is built with the transposing LDS read (ds_read_b64_tr_b16).
 //   Both buffers are XOR-swizzled by row so the read patterns spread over all
 //   LDS banks.
 // * Rows are gathered through the memory's logical->slot table; a tile may
-//   straddle entries and the current chunk.  The entry of the tile's first
-//   row is tracked per wave; each lane resolves its own row from it.  Rows
-//   past the last key load the last key again and score -inf.
+//   straddle two entries and the current chunk.  Row addresses come from
+//   two wave-uniform entry bases per tile (entries of at least 64 rows), or
+//   from a per-row lookup (shorter entries).  Rows past the last key load the
+//   last key again and score -inf.
 // * Online softmax in base 2 with the scale folded into one FMA; O is
 //   rescaled only when a row max grows by more than 2^8 (the stale max
 //   cancels in the final normalisation).  The denominator sums the
 //   bf16-rounded weights that enter the P.V product.
-// * Workgroup index -> share is remapped so that consecutive shares (the
-//   query tiles of one head) run on the same XCD and share its L2.
+// * Workgroup index -> work is remapped so that one XCD runs a contiguous
+//   range of (head, query tile) and shares K/V in its L2.
 #include <mutex>
+#include <type_traits>
 
 #include "fademem_internal.h"
 
@@ -77,11 +82,15 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
 constexpr int kThreads = kAttnThreads;
-constexpr int kBM = kAttnQueries;  // queries per workgroup (4 waves x 32)
+constexpr int kWaves = kThreads / 64;
+constexpr int kBM = kAttnQueries;  // queries per workgroup
+constexpr int kQW = kBM / kWaves;  // queries per wave
+constexpr int QB = kQW / 32;       // 32-query blocks per wave
 constexpr int kBN = 64;            // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kRescaleLog2 = 8.0f;  // rescale O when the max grows by > 2^8
+constexpr float kRescaleBound = 256.0f;  // redo a tile whose weights exceed 2^8
+static_assert(QB * 32 == kQW && (QB == 1 || QB == 2), "32-query blocks per wave");
 
 template <int D>
 struct Shape {
@@ -92,7 +101,7 @@ struct Shape {
   static constexpr int TILE_BYTES = kBN * D * 2;
   static constexpr int LOADS = kBN * CH / kThreads;  // 16-byte loads per lane per tile (per K and V)
   static_assert(LOADS * kThreads == kBN * CH, "tile split");
-  static_assert(kBM * D == 4 * DB * 16 * 64, "scratch slot holds the four waves' O registers");
+  static_assert(kBM * D == kWaves * QB * DB * 16 * 64, "scratch slot holds every wave's O registers");
 };
 
 // Swizzles: LDS 16-byte position of chunk c of row n is c ^ swz(n).
@@ -108,22 +117,30 @@ __device__ __forceinline__ int vswz(int n) {
 // Round two weights to bf16 and add the ROUNDED values to an fp32 sum in one
 // v_dot2 against (1, 1): the denominator then sums exactly the weights the
 // P.V product uses, so O is a convex combination of V rows.
-__device__ __forceinline__ bf16x2 round_and_sum(float p0, float p1, float& sum) {
+__device__ __forceinline__ uint32_t round_and_sum(float p0, float p1, float& sum) {
   bf16x2 pk;
   pk[0] = (__bf16)p0;
   pk[1] = (__bf16)p1;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   sum = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, sum, false);
-  return pk;
+  return __builtin_bit_cast(uint32_t, pk);
 }
 
 __device__ __forceinline__ float pair_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float pair_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// A pointer the whole wave holds, moved to scalar registers.
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+  return reinterpret_cast<const char*>((uint64_t(hi) << 32) | lo);
 }
 
 // XCD-aware group index: blocks are dealt to the 8 XCDs round-robin, so
@@ -134,8 +151,9 @@ __device__ __forceinline__ int xcd_group(int bid, int groups) {
   return (xcd < rem) ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
 }
 
-// Final output of one lane: O row (query q_row, head h) from the O^T
-// accumulators divided by the row sum, and the row's LSE.
+// Final output of one lane for one 32-query block: O row (query q_row,
+// head h) from the O^T accumulators divided by the row sum, and the row's
+// LSE.
 template <int D>
 __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (&o)[Shape<D>::DB], float m_scaled,
                                           float l_tot, int q_row, int h, int hh) {
@@ -157,16 +175,23 @@ __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (
   if (args.lse && hh == 0) args.lse[size_t(h) * Lq + q_row] = (m_scaled + __log2f(l_tot)) * kLn2;
 }
 
+// Scratch slot layout of a partial result: O registers lane-major,
+// [wave][qb][db][r][lane], then m and l per (qb, thread).
 template <int D>
+__device__ __forceinline__ size_t ws_o_index(int wave, int qb, int db, int r, int lane) {
+  return ((size_t((wave * QB + qb) * Shape<D>::DB + db) * 16 + r) * 64 + lane);
+}
+
+template <int D, bool WIDE>
 __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const SkPlan& plan) {
   using S = Shape<D>;
-  // Tile buffers: separate LDS objects, so the compiler can tell the reads
-  // of one buffer from the in-flight direct-to-LDS loads into the other and
-  // does not wait for those loads before reading.
+  // Three-deep rings of K and V tile buffers, each a separate LDS object.
   __shared__ __attribute__((aligned(16))) char k_lds0[S::TILE_BYTES];
-  __shared__ __attribute__((aligned(16))) char v_lds0[S::TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char k_lds1[S::TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) char k_lds2[S::TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) char v_lds0[S::TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char v_lds1[S::TILE_BYTES];
+  __shared__ __attribute__((aligned(16))) char v_lds2[S::TILE_BYTES];
   // Entry table: K address of row 0 (head 0) of each memory entry, and the
   // current chunk as entry n_entries; V is v_offset (memory) or v_cur-k_cur
   // (current chunk) bytes further.
@@ -175,7 +200,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
 
   const int g = xcd_group(blockIdx.x, gridDim.x);
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int l32 = lane & 31;
   const int hh = lane >> 5;
@@ -183,32 +208,36 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
   const int H = args.heads;
   const int n_entries = int(args.n_entries);
   const int N = int(args.tokens_per_block);
-  const int Lk = n_entries * N + int(args.cur_tokens);
+  const int cur_tokens = int(args.cur_tokens);
+  const int Lk = n_entries * N + cur_tokens;
   const int Lq = int(args.q_tokens);
   const size_t row_bytes = size_t(H) * D * 2;
   const char* k_cur = static_cast<const char*>(args.k_cur);
   const long long mem_vdelta = (long long)args.v_offset;
   const long long cur_vdelta = static_cast<const char*>(args.v_cur) - k_cur;
+  const int mem_rows = n_entries * N;
 
   for (int e = tid; e < n_entries + 1; e += kThreads)
     ent_k[e] = (e < n_entries) ? args.kv_layer_base + size_t(args.order[e]) * args.slot_stride : k_cur;
 
-  const bool wide = N >= kBN;  // then a tile spans at most two entries
-  const double inv_n = 1.0 / double(N);
-  const int mem_rows = n_entries * N;
-
   // Per-lane constants of the tile loads: load i writes destination chunk
-  // q = (4i + wave)*64 + lane = row n0, LDS position p; it fetches global
+  // q = (i*waves + wave)*64 + lane = row n0, LDS position p; it fetches global
   // chunk p ^ swz(n0) of that row.
-  int ld_row[S::LOADS];
+  auto ld_row = [&](int i) { return ((i * kWaves + wave) * 64 + lane) / S::CH; };
+  auto ld_kch = [&](int i) {
+    const int q = (i * kWaves + wave) * 64 + lane;
+    return uint32_t(((q % S::CH) ^ kswz<D>(q / S::CH)) * 16);
+  };
+  auto ld_vch = [&](int i) {
+    const int q = (i * kWaves + wave) * 64 + lane;
+    return uint32_t(((q % S::CH) ^ vswz<D>(q / S::CH)) * 16);
+  };
+  // Byte offsets from a tile's first row to this lane's K and V chunks.
   uint32_t ld_koff[S::LOADS], ld_voff[S::LOADS];
 #pragma unroll
   for (int i = 0; i < S::LOADS; ++i) {
-    const int q = (i * 4 + wave) * 64 + lane;
-    const int n0 = q / S::CH, p = q % S::CH;
-    ld_row[i] = n0;
-    ld_koff[i] = uint32_t(size_t(n0) * row_bytes) + uint32_t((p ^ kswz<D>(n0)) * 16);
-    ld_voff[i] = uint32_t(size_t(n0) * row_bytes) + uint32_t((p ^ vswz<D>(n0)) * 16);
+    ld_koff[i] = uint32_t(size_t(ld_row(i)) * row_bytes) + ld_kch(i);
+    ld_voff[i] = uint32_t(size_t(ld_row(i)) * row_bytes) + ld_vch(i);
   }
 
   // Per-lane LDS read offsets (loop-invariant; the buffer and the (nb, ks)
@@ -232,216 +261,448 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
   }
   const float c2 = args.scale * kLog2e;
 
+  char* const kbuf[3] = {k_lds0, k_lds1, k_lds2};
+  char* const vbuf[3] = {v_lds0, v_lds1, v_lds2};
+
   // One query tile's key tiles [kt0, kt1); the result goes to the output
   // (slot < 0, the range is the whole key axis) or, partial, to scratch slot
   // `slot`.
   auto segment = [&](int h, int qt, int kt0, int kt1, int slot) {
     const size_t head_off = size_t(h) * D * 2;
-    auto entry_base = [&](int e, const char*& kb, long long& vd) {
-      kb = ent_k[e] + head_off;
-      vd = (e < n_entries) ? mem_vdelta : cur_vdelta;
-    };
 
-    // Q fragment (B operand of S^T = K Q^T): query m = l32, d = 16*kb + 8*hh + 0..7.
-    const int q_row = qt * kBM + wave * 32 + l32;
-    bf16x8 qf[S::KB];
-    {
+    // Q fragments (B operand of S^T = K Q^T): query m = l32 of block qb,
+    // d = 16*kb + 8*hh + 0..7.
+    bf16x8 qf[QB][S::KB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const int q_row = qt * kBM + wave * kQW + 32 * qb + l32;
       const char* qbase = static_cast<const char*>(args.q) + (size_t(q_row < Lq ? q_row : Lq - 1) * H + h) * D * 2;
 #pragma unroll
-      for (int kb = 0; kb < S::KB; ++kb) qf[kb] = *reinterpret_cast<const bf16x8*>(qbase + (16 * kb + 8 * hh) * 2);
+      for (int kb = 0; kb < S::KB; ++kb)
+        qf[qb][kb] = *reinterpret_cast<const bf16x8*>(qbase + (16 * kb + 8 * hh) * 2);
     }
 
-    // Tile t's first row lies in entry e0 at row off0 (e0 == n_entries: the
-    // current chunk, which is never wrapped).
-    int e0, off0;
-    auto locate = [&](int k0) {
-      if (k0 < mem_rows) {
-        e0 = k0 / N;
-        off0 = k0 - e0 * N;
-      } else {
-        e0 = n_entries;
-        off0 = k0 - mem_rows;
-      }
-    };
-    locate(kt0 * kBN);
-
-    // Issue the global->LDS loads of tile `tile` into the given buffers.
-    auto issue_tile = [&](int tile, char* kb_lds, char* vb_lds) {
-      const int k0 = tile * kBN;
-      if (wide && k0 + kBN <= Lk) {
-        // Rows n < ncross are entry e0's rows off0 + n; the rest are entry
-        // e0+1's rows n - ncross.  Row n's address = base + n*row_bytes.
-        const char* kb0;
-        const char* kb1;
-        long long vd0, vd1;
-        entry_base(e0, kb0, vd0);
-        entry_base(e0 + 1 <= n_entries ? e0 + 1 : n_entries, kb1, vd1);
-        const int ncross = (e0 < n_entries) ? N - off0 : kBN;
-        const char* base0 = kb0 + (long long)off0 * (long long)row_bytes;
-        const char* base1 = kb1 - (long long)ncross * (long long)row_bytes;
-#pragma unroll
-        for (int i = 0; i < S::LOADS; ++i) {
-          const bool cross = ld_row[i] >= ncross;
-          const char* kb = cross ? base1 : base0;
-          const char* vb = cross ? base1 + vd1 : base0 + vd0;
-          const int j = i * 4 + wave;
-          __builtin_amdgcn_global_load_lds(kb + ld_koff[i], (LDS_AS void*)(kb_lds + j * 1024), 16, 0, 0);
-          __builtin_amdgcn_global_load_lds(vb + ld_voff[i], (LDS_AS void*)(vb_lds + j * 1024), 16, 0, 0);
-        }
-      } else {
-        // General rows (last tile, or entries shorter than a tile): resolve
-        // each row by division; rows past the last key reload the last key.
-#pragma unroll
-        for (int i = 0; i < S::LOADS; ++i) {
-          const int q = (i * 4 + wave) * 64 + lane;
-          const int n0 = q / S::CH, p = q % S::CH;
-          const int k = (k0 + n0 < Lk) ? k0 + n0 : Lk - 1;
-          int e = int((double(k) + 0.5) * inv_n);
-          if (e > n_entries) e = n_entries;
-          const bool in_mem = k < mem_rows;
-          const int off = in_mem ? k - e * N : k - mem_rows;
-          const char* kb;
-          long long vd;
-          entry_base(in_mem ? e : n_entries, kb, vd);
-          const char* krow = kb + size_t(off) * row_bytes;
-          const int j = i * 4 + wave;
-          __builtin_amdgcn_global_load_lds(krow + (p ^ kswz<D>(n0)) * 16, (LDS_AS void*)(kb_lds + j * 1024), 16, 0,
-                                           0);
-          __builtin_amdgcn_global_load_lds(krow + vd + (p ^ vswz<D>(n0)) * 16, (LDS_AS void*)(vb_lds + j * 1024), 16,
-                                           0, 0);
-        }
-      }
-    };
-    auto advance_tile_start = [&](int next_k0) {
-      if (wide) {
-        off0 += kBN;
-        if (e0 < n_entries && off0 >= N) {
-          off0 -= N;
-          ++e0;
-        }
-      } else {
-        locate(next_k0);
-      }
-    };
-
-    f32x16 o[S::DB];
-#pragma unroll
-    for (int db = 0; db < S::DB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-    float m_run = -INFINITY;  // running (possibly stale) max of raw scores for query l32
-    float l_run = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2)
-
-    // One tile: wait for its loads, start the next tile's loads into the
-    // other buffers, then S^T = K Q^T, online softmax, O^T += V^T P^T.
-    auto step = [&](int tile, const char* kb_lds, const char* vb_lds, char* next_k, char* next_v) {
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();  // tile landed for every wave; the other buffers are free
-      if (tile + 1 < kt1) {
-        advance_tile_start((tile + 1) * kBN);
-        issue_tile(tile + 1, next_k, next_v);
-      }
-
-      f32x16 s[2];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[nb][r] = 0.0f;
-      {
-        bf16x8 ka[2][2];  // [nb][k-step parity]: fragments read one k-step ahead
-        ka[0][0] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[0]);
-        ka[1][0] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[0] + 32 * D * 2);
-#pragma unroll
-        for (int kb = 0; kb < S::KB; ++kb) {
-          if (kb + 1 < S::KB) {
-            ka[0][(kb + 1) & 1] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb + 1]);
-            ka[1][(kb + 1) & 1] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb + 1] + 32 * D * 2);
-          }
-          s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[0][kb & 1], qf[kb], s[0], 0, 0, 0);
-          s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[1][kb & 1], qf[kb], s[1], 0, 0, 0);
-        }
-      }
-      const int k0 = tile * kBN;
-      if (k0 + kBN > Lk) {
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + 32 * nb + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (key >= Lk) s[nb][r] = -INFINITY;
-          }
-      }
-      float mx;
-      {
-        float m8[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) m8[i] = fmaxf(fmaxf(s[0][i], s[0][i + 8]), fmaxf(s[1][i], s[1][i + 8]));
-#pragma unroll
-        for (int w = 4; w >= 1; w >>= 1)
-#pragma unroll
-          for (int i = 0; i < w; ++i) m8[i] = fmaxf(m8[i], m8[i + w]);
-        mx = pair_max(m8[0]);
-      }
-      if (__any((mx - m_run) * c2 > kRescaleLog2)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-        m_run = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < S::DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      }
-      const float mc = m_run * c2;
-      float ps[4] = {0.f, 0.f, 0.f, 0.f};
-      u32x4 pw[4];  // P as packed bf16 pairs: k-step 2*nb + r/8, word (r%8)/2
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][r], c2, -mc));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][r + 1], c2, -mc));
-          pw[2 * nb + (r >> 3)][(r & 7) >> 1] = __builtin_bit_cast(uint32_t, round_and_sum(p0, p1, ps[(r >> 1) & 3]));
-        }
-      }
-      l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
-
-#pragma unroll
-      for (int db = 0; db < S::DB; ++db) {
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-          bf16x8 a;
-#pragma unroll
-          for (int second = 0; second < 2; ++second) {
-            const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (LDS_AS s16x4*)((LDS_AS const char*)(vb_lds) + v_rd[db] + (16 * ks + 8 * second) * D * 2));
-            const bf16x4 vb = __builtin_bit_cast(bf16x4, v);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) a[4 * second + e] = vb[e];
-          }
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, pw[ks]), o[db], 0, 0, 0);
-        }
-      }
-    };
-
-    __syncthreads();  // entry table visible; the previous segment's reads of the buffers are done
-    issue_tile(kt0, k_lds0, v_lds0);
-    for (int tile = kt0; tile < kt1; tile += 2) {
-      step(tile, k_lds0, v_lds0, k_lds1, v_lds1);
-      if (tile + 1 < kt1) step(tile + 1, k_lds1, v_lds1, k_lds0, v_lds0);
-    }
-
-    if (slot < 0) {
-      store_out<D>(args, o, m_run * c2, pair_sum(l_run), q_row, h, hh);
+    // Address of the last key's row (rows past the last key load it again).
+    const char* last_k;
+    long long last_vd;
+    if (cur_tokens > 0) {
+      last_k = k_cur + size_t(cur_tokens - 1) * row_bytes + head_off;
+      last_vd = cur_vdelta;
     } else {
-      // Partial: the O^T registers lane-major, then per-thread m and l.
-      float* ws = args.ws + size_t(slot) * attend_slot_floats(D);
+      last_k = ent_k[n_entries - 1] + size_t(N - 1) * row_bytes + head_off;
+      last_vd = mem_vdelta;
+    }
+
+    // Load stream: the next tile to load starts in entry ld_e at row ld_off
+    // (ld_e == n_entries: the current chunk).
+    int ld_e, ld_off;
+    {
+      const int k0 = kt0 * kBN;
+      if (k0 < mem_rows) {
+        ld_e = k0 / N;
+        ld_off = k0 - ld_e * N;
+      } else {
+        ld_e = n_entries;
+        ld_off = k0 - mem_rows;
+      }
+    }
+    // Wave-uniform part of one tile's row addresses (entries of >= 64 rows:
+    // rows n < ncross are entry ld_e's rows ld_off + n, the rest are entry
+    // ld_e+1's rows n - ncross); advances the stream by one tile.
+    struct TileRows {
+      const char* base0;
+      const char* base1;
+      long long vd0, vd1;
+      int ncross, nvalid, k0;
+    };
+    auto tile_rows = [&](int tile) {
+      TileRows tr;
+      tr.k0 = tile * kBN;
+      tr.nvalid = Lk - tr.k0;
+      if constexpr (WIDE) {
+        const int e1 = ld_e + 1 <= n_entries ? ld_e + 1 : n_entries;
+        const bool in_mem0 = ld_e < n_entries;
+        tr.ncross = in_mem0 ? N - ld_off : kBN;
+        tr.base0 = ent_k[ld_e] + head_off + (long long)ld_off * (long long)row_bytes;
+        tr.base1 = ent_k[e1] + head_off - (long long)tr.ncross * (long long)row_bytes;
+        tr.vd0 = in_mem0 ? mem_vdelta : cur_vdelta;
+        tr.vd1 = e1 < n_entries ? mem_vdelta : cur_vdelta;
+        ld_off += kBN;
+        if (in_mem0 && ld_off >= N) {
+          ld_off -= N;
+          ++ld_e;
+        }
+      }
+      return tr;
+    };
+    // Load i (K and V) of a tile into the given buffers.
+    auto load_one = [&](const TileRows& tr, int i, char* kb_lds, char* vb_lds) {
+      const char* row;
+      long long vd;
+      if constexpr (WIDE) {
+        const int n = ld_row(i);
+        const bool cross = n >= tr.ncross;
+        const bool valid = n < tr.nvalid;
+        row = valid ? (cross ? tr.base1 : tr.base0) + size_t(n) * row_bytes : last_k;
+        vd = valid ? (cross ? tr.vd1 : tr.vd0) : last_vd;
+      } else {
+        // Entries shorter than a tile: resolve the row on its own.
+        const int k = tr.k0 + ld_row(i);
+        if (k >= Lk) {
+          row = last_k;
+          vd = last_vd;
+        } else if (k < mem_rows) {
+          const int e = k / N;
+          row = ent_k[e] + head_off + size_t(k - e * N) * row_bytes;
+          vd = mem_vdelta;
+        } else {
+          row = k_cur + head_off + size_t(k - mem_rows) * row_bytes;
+          vd = cur_vdelta;
+        }
+      }
+      const int j = i * kWaves + wave;
+      __builtin_amdgcn_global_load_lds(row + ld_kch(i), (LDS_AS void*)(kb_lds + j * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(row + vd + ld_vch(i), (LDS_AS void*)(vb_lds + j * 1024), 16, 0, 0);
+    };
+    // All loads of a tile.  A full tile inside one entry (the common case)
+    // takes its rows from one wave-uniform base plus the lane's fixed
+    // offsets, so its addresses cost no vector instructions.
+    auto load_tile = [&](const TileRows& tr, char* kb_lds, char* vb_lds) {
+      if constexpr (WIDE) {
+        if (tr.ncross >= kBN && tr.nvalid >= kBN) {
+          const char* kbase = uniform_ptr(tr.base0);
+          const char* vbase = uniform_ptr(tr.base0 + tr.vd0);
+#pragma unroll
+          for (int i = 0; i < S::LOADS; ++i) {
+            const int j = i * kWaves + wave;
+            __builtin_amdgcn_global_load_lds(kbase + ld_koff[i], (LDS_AS void*)(kb_lds + j * 1024), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(vbase + ld_voff[i], (LDS_AS void*)(vb_lds + j * 1024), 16, 0, 0);
+          }
+          return;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < S::LOADS; ++i) load_one(tr, i, kb_lds, vb_lds);
+    };
+    auto issue_tile = [&](int tile, char* kb_lds, char* vb_lds) { load_tile(tile_rows(tile), kb_lds, vb_lds); };
+
+    f32x16 o[QB][S::DB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
       for (int db = 0; db < S::DB; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ws[((wave * S::DB + db) * 16 + r) * 64 + lane] = o[db][r];
-      ws[kBM * D + tid] = m_run;
-      ws[kBM * D + kThreads + tid] = l_run;
+        for (int r = 0; r < 16; ++r) o[qb][db][r] = 0.0f;
+    float m_run[QB], l_run[QB];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      m_run[qb] = -INFINITY;  // running (possibly stale) max of raw scores
+      l_run[qb] = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2)
+    }
+
+    const int partial_tile = (Lk % kBN) ? (Lk / kBN) : -1;  // the tile with keys >= Lk, if any
+    f32x16 s_cur[2][QB];  // S^T of the current tile [nb][qb]
+    u32x4 p_cur[4][QB];   // P of the current tile [ks][qb] (bf16 pairs)
+    float ps_cur[QB];     // this lane's sum of the current tile's P so far
+
+    // Softmax without a per-tile row max: a tile's weights are taken against
+    // the running max m_run as it stands.  If any weight of a row exceeds
+    // 2^8 (seen as the lane's tile sum exceeding 2^8: every weight is at most
+    // the sum), the tile is redone against the exact new max and O and l are
+    // rescaled; otherwise every weight stays <= 2^8 and the stale m_run
+    // cancels in the final normalisation.
+    //
+    // Score pair pi (0..kPairs-1) of a tile: query block qb = pi/16, rows
+    // r, r+1 of accumulator block nb.  Pairs [0, kPairsB) are exponentiated
+    // in block B, the rest in the next block A.
+    constexpr int kPairs = 16 * QB;
+    constexpr int kPairsB = 8 * QB;
+    auto exp_pair = [&](const f32x16 (&s)[2][QB], u32x4 (&p)[4][QB], float (&ps)[QB], int pi) {
+      const int qb = pi / 16, rr = pi % 16, nb = rr / 8, r = 2 * (rr % 8);
+      const float mc = m_run[qb] * c2;
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r], c2, -mc));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r + 1], c2, -mc));
+      const uint32_t w = round_and_sum(p0, p1, ps[qb]);
+      asm volatile("" ::"v"(w));  // keep the weight in its pipeline step
+      p[2 * nb + (r >> 3)][qb][(r & 7) >> 1] = w;
+    };
+    // Mask keys >= Lk of a tile to -inf.
+    auto mask = [&](int tile, f32x16 (&s)[2][QB]) {
+      const int k0 = tile * kBN;
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * nb + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (key >= Lk) s[nb][qb][r] = -INFINITY;
+          }
+    };
+    // Row max of a tile's scores (v_maximum3: NaN-propagating, so the raw
+    // MFMA results need no canonicalisation), reduced over the lane pair.
+    auto row_max = [&](const f32x16 (&s)[2][QB], float (&mx)[QB]) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float m0 = s[0][qb][0], m1 = s[1][qb][0];
+#pragma unroll
+        for (int r = 1; r < 15; r += 2) {
+          m0 = __builtin_elementwise_maximum(m0, __builtin_elementwise_maximum(s[0][qb][r], s[0][qb][r + 1]));
+          m1 = __builtin_elementwise_maximum(m1, __builtin_elementwise_maximum(s[1][qb][r], s[1][qb][r + 1]));
+        }
+        mx[qb] = pair_max(__builtin_elementwise_maximum(m0, __builtin_elementwise_maximum(m1, __builtin_elementwise_maximum(
+                                                                                                 s[0][qb][15], s[1][qb][15]))));
+      }
+    };
+    // S^T of a tile from its K buffer (masked if it is the partial tile).
+    auto qk_tile = [&](int tile, const char* kb_lds, f32x16 (&s)[2][QB]) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s[nb][qb][r] = 0.0f;
+#pragma unroll
+      for (int kb = 0; kb < S::KB; ++kb) {
+        const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb]);
+        const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb] + 32 * D * 2);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+          s[0][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[qb][kb], s[0][qb], 0, 0, 0);
+          s[1][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[qb][kb], s[1][qb], 0, 0, 0);
+        }
+      }
+      if (tile == partial_tile) mask(tile, s);
+    };
+    // Redo a tile against the exact running max: its scores again from its K
+    // buffer, new m_run, rescale O and l, recompute all its weights and the
+    // tile sum.
+    auto redo_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
+      f32x16 s[2][QB];
+      qk_tile(tile, kb_lds, s);
+      float mx[QB];
+      row_max(s, mx);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const float m_new = __builtin_elementwise_maximum(m_run[qb], mx[qb]);
+        const float alpha = __builtin_amdgcn_exp2f((m_run[qb] - m_new) * c2);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < S::DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[qb][db][r] *= alpha;
+        ps[qb] = 0.0f;
+      }
+#pragma unroll
+      for (int pi = 0; pi < kPairs; ++pi) exp_pair(s, p, ps, pi);
+    };
+    // End of a tile's weights: redo it if a weight grew past 2^8, then add
+    // its sum to l.
+    auto close_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
+      bool grow = false;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) grow = grow || !(ps[qb] <= kRescaleBound);
+      if (__any(grow)) redo_tile(tile, kb_lds, p, ps);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) l_run[qb] += ps[qb];
+    };
+    auto read_k = [&](const char* kb_lds, int kb, bf16x8 (&kf)[2]) {
+      kf[0] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb]);
+      kf[1] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb] + 32 * D * 2);
+    };
+    // V^T fragment of k-step ks, 32-row block db (two transposing reads).
+    auto read_v = [&](const char* vb_lds, int ks, int db) {
+      bf16x8 a;
+#pragma unroll
+      for (int second = 0; second < 2; ++second) {
+        const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (LDS_AS s16x4*)((LDS_AS const char*)(vb_lds) + v_rd[db] + (16 * ks + 8 * second) * D * 2));
+        const bf16x4 vb = __builtin_bit_cast(bf16x4, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a[4 * second + e] = vb[e];
+      }
+      return a;
+    };
+    constexpr int kStepsB = 2 * S::DB;                // block B steps: (ks, pair of 32-row blocks)
+    constexpr int kDbPerStep = S::DB * 4 / kStepsB;   // = 2
+    constexpr int kPrefetch = 1;                      // steps between an LDS read and its MFMA
+
+    // One pipeline iteration for tile t (ring slot b): boundary, block A,
+    // tile t's weight check, block B.  LOAD: tile t+2 exists (its loads are
+    // issued); NEXT: tile t+1 exists; maskn: tile t+1 has keys >= Lk.
+    auto iteration = [&](int t, auto b_c, auto load_c, auto next_c, bool maskn) {
+      constexpr int b = decltype(b_c)::value;
+      constexpr bool LOAD = decltype(load_c)::value;
+      constexpr bool NEXT = decltype(next_c)::value;
+      const char* kb_next = kbuf[(b + 1) % 3];
+      const char* vb_cur = vbuf[b];
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();  // tiles t, t+1 landed for every wave; tile t-1's buffers are free
+      TileRows tr;
+      if constexpr (LOAD) tr = tile_rows(t + 2);
+
+      // Block A: S(t+1) = K(t+1) Q^T, one k-step per step, beside the loads
+      // of tile t+2 and the weights of S(t)'s pairs [kPairsB, kPairs).  The
+      // LDS reads of step st + kPrefetch are issued in step st (block A's
+      // last steps prefetch block B's first V^T fragments).
+      f32x16 s_next[2][QB];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) s_next[nb][qb][r] = 0.0f;
+      bf16x8 kring[kPrefetch + 1][2];
+      bf16x8 vring[kPrefetch + 1][kDbPerStep];
+      if constexpr (NEXT) {
+#pragma unroll
+        for (int j = 0; j < kPrefetch && j < S::KB; ++j) read_k(kb_next, j, kring[j]);
+      }
+#pragma unroll
+      for (int st = 0; st < S::KB; ++st) {
+        if constexpr (NEXT) {
+          if (st + kPrefetch < S::KB) read_k(kb_next, st + kPrefetch, kring[(st + kPrefetch) % (kPrefetch + 1)]);
+        }
+        {
+          const int j = st + kPrefetch - S::KB;  // block B step to prefetch
+          if (j >= 0 && j < kStepsB) {
+#pragma unroll
+            for (int d = 0; d < kDbPerStep; ++d)
+              vring[j % (kPrefetch + 1)][d] =
+                  read_v(vb_cur, j / (S::DB / kDbPerStep), (j % (S::DB / kDbPerStep)) * kDbPerStep + d);
+          }
+        }
+        if constexpr (LOAD) {
+          if (st == 0) load_tile(tr, kbuf[(b + 2) % 3], vbuf[(b + 2) % 3]);
+        }
+        if constexpr (NEXT) {
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+              s_next[nb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kring[st % (kPrefetch + 1)][nb], qf[qb][st],
+                                                                      s_next[nb][qb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int pi = kPairsB; pi < kPairs; ++pi)
+          if (st == (pi - kPairsB) * S::KB / (kPairs - kPairsB)) exp_pair(s_cur, p_cur, ps_cur, pi);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      close_tile(t, kbuf[b], p_cur, ps_cur);  // tile t's K buffer is refilled only in the next block A
+      __builtin_amdgcn_sched_barrier(0);
+
+      // Block B: O += V(t) P(t), two 32-row blocks of one k-step per step,
+      // beside the weights of S(t+1)'s pairs [0, kPairsB).
+      if constexpr (NEXT) {
+        if (maskn) mask(t + 1, s_next);
+      }
+      u32x4 p_next[4][QB];
+      float ps_next[QB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) ps_next[qb] = 0.0f;
+#pragma unroll
+      for (int st = 0; st < kStepsB; ++st) {
+        const int ks = st / (S::DB / kDbPerStep), db0 = (st % (S::DB / kDbPerStep)) * kDbPerStep;
+        if (st + kPrefetch < kStepsB) {
+          const int j = st + kPrefetch;
+#pragma unroll
+          for (int d = 0; d < kDbPerStep; ++d)
+            vring[j % (kPrefetch + 1)][d] =
+                read_v(vb_cur, j / (S::DB / kDbPerStep), (j % (S::DB / kDbPerStep)) * kDbPerStep + d);
+        }
+#pragma unroll
+        for (int d = 0; d < kDbPerStep; ++d)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            o[qb][db0 + d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                vring[st % (kPrefetch + 1)][d], __builtin_bit_cast(bf16x8, p_cur[ks][qb]), o[qb][db0 + d], 0, 0, 0);
+        if constexpr (NEXT) {
+#pragma unroll
+          for (int pi = 0; pi < kPairsB; ++pi)
+            if (st == pi * kStepsB / kPairsB) exp_pair(s_next, p_next, ps_next, pi);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (NEXT) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) s_cur[nb][qb] = s_next[nb][qb];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) p_cur[ks][qb] = p_next[ks][qb];
+          ps_cur[qb] = ps_next[qb];
+        }
+      }
+    };
+
+    // Prologue: tiles kt0 and kt0+1 into ring slots 0 and 1; S(kt0), its
+    // exact row max and its first kPairsB weights.
+    __syncthreads();  // entry table visible; the previous segment's reads of the buffers are done
+    issue_tile(kt0, kbuf[0], vbuf[0]);
+    if (kt0 + 1 < kt1) issue_tile(kt0 + 1, kbuf[1], vbuf[1]);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    {
+      qk_tile(kt0, kbuf[0], s_cur);
+      row_max(s_cur, m_run);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) ps_cur[qb] = 0.0f;
+#pragma unroll
+      for (int pi = 0; pi < kPairsB; ++pi) exp_pair(s_cur, p_cur, ps_cur, pi);
+    }
+
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using T = std::true_type;
+    using F = std::false_type;
+    int t = kt0;
+    while (true) {
+      if (t + 2 >= kt1) break;
+      iteration(t, I0{}, T{}, T{}, false);
+      ++t;
+      if (t + 2 >= kt1) break;
+      iteration(t, I1{}, T{}, T{}, false);
+      ++t;
+      if (t + 2 >= kt1) break;
+      iteration(t, I2{}, T{}, T{}, false);
+      ++t;
+    }
+    // The last one or two tiles (no loads left to issue).
+    if (t + 1 < kt1) {
+      const int b = (t - kt0) % 3;
+      const bool mk = (t + 1 == partial_tile);
+      if (b == 0) iteration(t, I0{}, F{}, T{}, mk);
+      else if (b == 1) iteration(t, I1{}, F{}, T{}, mk);
+      else iteration(t, I2{}, F{}, T{}, mk);
+      ++t;
+    }
+    {
+      const int b = (t - kt0) % 3;
+      if (b == 0) iteration(t, I0{}, F{}, F{}, false);
+      else if (b == 1) iteration(t, I1{}, F{}, F{}, false);
+      else iteration(t, I2{}, F{}, F{}, false);
+    }
+    // (The last tile's rescale was applied at its boundary.)
+    if (slot < 0) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+        store_out<D>(args, o[qb], m_run[qb] * c2, pair_sum(l_run[qb]), qt * kBM + wave * kQW + 32 * qb + l32, h,
+                     hh);
+    } else {
+      float* ws = args.ws + size_t(slot) * attend_slot_floats(D);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+#pragma unroll
+        for (int db = 0; db < S::DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) ws[ws_o_index<D>(wave, qb, db, r, lane)] = o[qb][db][r];
+        ws[kBM * D + qb * kThreads + tid] = m_run[qb];
+        ws[kBM * D + (QB + qb) * kThreads + tid] = l_run[qb];
+      }
     }
   };
 
@@ -487,33 +748,44 @@ __device__ __forceinline__ void attend_bf16_merge_body(const AttendArgs& args, c
   const float c2 = args.scale * kLog2e;
   const float* part[2] = {args.ws + size_t(i) * attend_slot_floats(D),
                           args.ws + size_t(plan.rem + i) * attend_slot_floats(D)};
-  const float m_max = fmaxf(part[0][kBM * D + tid], part[1][kBM * D + tid]);
-  f32x16 o[S::DB];
 #pragma unroll
-  for (int db = 0; db < S::DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-  float l_tot = 0.0f;
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const float* ws = part[p];
-    const float f = __builtin_amdgcn_exp2f((ws[kBM * D + tid] - m_max) * c2);
-    l_tot += f * pair_sum(ws[kBM * D + kThreads + tid]);
+  for (int qb = 0; qb < QB; ++qb) {
+    const int mi = kBM * D + qb * kThreads + tid, li = kBM * D + (QB + qb) * kThreads + tid;
+    const float m_max = fmaxf(part[0][mi], part[1][mi]);
+    f32x16 o[S::DB];
 #pragma unroll
     for (int db = 0; db < S::DB; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] += f * ws[((wave * S::DB + db) * 16 + r) * 64 + lane];
+      for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+    float l_tot = 0.0f;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const float* ws = part[p];
+      const float f = __builtin_amdgcn_exp2f((ws[mi] - m_max) * c2);
+      l_tot += f * pair_sum(ws[li]);
+#pragma unroll
+      for (int db = 0; db < S::DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] += f * ws[ws_o_index<D>(wave, qb, db, r, lane)];
+    }
+    store_out<D>(args, o, m_max * c2, l_tot, (qg % plan.q_tiles) * kBM + wave * kQW + 32 * qb + l32,
+                 qg / plan.q_tiles, hh);
   }
-  store_out<D>(args, o, m_max * c2, l_tot, (qg % plan.q_tiles) * kBM + wave * 32 + l32, qg / plan.q_tiles, hh);
 }
 
 }  // namespace
 
-__global__ __launch_bounds__(kThreads, 2) void attend_bf16_d128(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128>(args, plan);
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<128, true>(args, plan);
 }
-__global__ __launch_bounds__(kThreads, 2) void attend_bf16_d64(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64>(args, plan);
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<64, true>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_short(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<128, false>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_short(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<64, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads) void attend_bf16_merge_d128(AttendArgs args, SkPlan plan) {
   attend_bf16_merge_body<128>(args, plan);
@@ -524,8 +796,9 @@ __global__ __launch_bounds__(kThreads) void attend_bf16_merge_d64(AttendArgs arg
 
 namespace {
 
-template <typename Kernel>
-hipError_t launch_d(Kernel kernel, Kernel merge, std::once_flag& attr_once, const AttendArgs& a,
+typedef void (*AttnKernel)(AttendArgs, SkPlan);
+
+hipError_t launch_d(AttnKernel kernel, AttnKernel merge, std::once_flag& attr_once, const AttendArgs& a,
                     hipStream_t stream) {
   const int64_t q_tiles64 = (a.q_tokens + kBM - 1) / kBM;
   if (q_tiles64 * a.heads > int64_t(0x7fffffff)) return hipErrorInvalidValue;
@@ -556,7 +829,9 @@ hipError_t launch_d(Kernel kernel, Kernel merge, std::once_flag& attr_once, cons
   plan.tails_per = plan.rem > 0 ? (plan.rem + (plan.groups - plan.rem) - 1) / (plan.groups - plan.rem) : 1;
   plan.tail_len = plan.tiles / (plan.tails_per + 1);
   plan.head_len = plan.tiles - plan.tail_len;
-  const int launched = plan.rounds > 0 ? plan.groups : plan.rem + (plan.tail_len > 0 ? (plan.rem + plan.tails_per - 1) / plan.tails_per : 0);
+  const int launched =
+      plan.rounds > 0 ? plan.groups
+                      : plan.rem + (plan.tail_len > 0 ? (plan.rem + plan.tails_per - 1) / plan.tails_per : 0);
   hipLaunchKernelGGL(kernel, dim3(launched), dim3(kThreads), shmem, stream, a, plan);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (plan.rem > 0 && plan.tail_len > 0) {
@@ -566,13 +841,18 @@ hipError_t launch_d(Kernel kernel, Kernel merge, std::once_flag& attr_once, cons
   return e;
 }
 
-std::once_flag attr_d128, attr_d64;
+std::once_flag attr_d128, attr_d64, attr_d128s, attr_d64s;
 
 }  // namespace
 
 hipError_t launch_attend_bf16(const AttendArgs& a, hipStream_t stream) {
-  if (a.head_dim == 128) return launch_d(attend_bf16_d128, attend_bf16_merge_d128, attr_d128, a, stream);
-  if (a.head_dim == 64) return launch_d(attend_bf16_d64, attend_bf16_merge_d64, attr_d64, a, stream);
+  const bool wide = a.tokens_per_block >= kBN;
+  if (a.head_dim == 128)
+    return wide ? launch_d(attend_bf16_d128, attend_bf16_merge_d128, attr_d128, a, stream)
+                : launch_d(attend_bf16_d128_short, attend_bf16_merge_d128, attr_d128s, a, stream);
+  if (a.head_dim == 64)
+    return wide ? launch_d(attend_bf16_d64, attend_bf16_merge_d64, attr_d64, a, stream)
+                : launch_d(attend_bf16_d64_short, attend_bf16_merge_d64, attr_d64s, a, stream);
   return hipErrorInvalidValue;
 }
 

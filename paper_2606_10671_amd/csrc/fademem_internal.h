@@ -16,16 +16,20 @@ constexpr int kMaxLayersPerLaunch = 64;   // layer pointers passed as kernel arg
 constexpr int64_t kMaxPosition = int64_t(1) << 40;
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
 
-// bf16 attention work split.  The key range of every query tile is cut into
-// equal shares for at most kSkMaxGroups resident workgroups; a share that
-// covers part of a query tile leaves a partial result (unnormalised O, row
-// max and row sums) in one of two scratch slots per workgroup, and a second
-// kernel merges the partials of each split tile.
-constexpr int kAttnThreads = 256;        // threads per workgroup (4 waves)
-constexpr int kAttnQueries = 128;        // queries per workgroup (32 per wave)
-constexpr int kSkMaxGroups = 512;        // workgroups of one launch at most
+// bf16 attention work split.  A workgroup (4 waves x 64 queries) runs one
+// query tile's key range, or part of it: when the tiles do not fill whole
+// rounds of resident workgroups, the remaining tiles are split along the key
+// axis between workgroups, each part leaves its partial result (unnormalised
+// O, row max and row sums) in a scratch slot, and a second kernel merges the
+// two parts of each split tile.  At most kSkMaxGroups workgroups per launch,
+// two scratch slots per workgroup.
+constexpr int kAttnThreads = 512;        // threads per workgroup (8 waves)
+constexpr int kAttnQueries = 256;        // queries per workgroup (32 per wave)
+constexpr int kSkMaxGroups = 256;        // workgroups of one launch at most (one per CU)
 __host__ __device__ constexpr size_t attend_slot_floats(int head_dim) {
-  return size_t(kAttnQueries) * size_t(head_dim) + 2 * size_t(kAttnThreads);
+  // O of every query, then the row max and the partial row sum of every
+  // (thread, 32-query block).
+  return size_t(kAttnQueries) * size_t(head_dim) + 4 * size_t(kAttnQueries);
 }
 __host__ __device__ constexpr size_t attend_ws_bytes(int head_dim) {
   return 2 * size_t(kSkMaxGroups) * attend_slot_floats(head_dim) * sizeof(float);
