@@ -19,14 +19,20 @@ import sys
 import time
 
 WORKLOADS = {
-    # name: heads, head_dim, tokens_per_block, frames_per_chunk, budget, layers, dtype
+    # name: heads, head_dim, tokens_per_block, frames_per_chunk, budget, layers, dtype, chunks (default run length)
     "wan1.3b-1layer": dict(heads=12, head_dim=128, tokens_per_block=1560, frames=3, budget=21, layers=1,
-                           dtype="bf16"),
+                           dtype="bf16", chunks=120),
     "wan1.3b-30layer": dict(heads=12, head_dim=128, tokens_per_block=1560, frames=3, budget=21, layers=30,
-                            dtype="bf16"),
+                            dtype="bf16", chunks=240),
+    # about an hour of video at 16 fps with a 4x temporal VAE
+    "wan1.3b-hour": dict(heads=12, head_dim=128, tokens_per_block=1560, frames=3, budget=21, layers=30,
+                         dtype="bf16", chunks=4800),
     "wan14b-1layer": dict(heads=40, head_dim=128, tokens_per_block=3600, frames=3, budget=21, layers=1,
-                          dtype="bf16"),
-    "tiny-fp32": dict(heads=2, head_dim=64, tokens_per_block=64, frames=1, budget=8, layers=1, dtype="f32"),
+                          dtype="bf16", chunks=120),
+    "wan14b-40layer": dict(heads=40, head_dim=128, tokens_per_block=3600, frames=3, budget=21, layers=40,
+                           dtype="bf16", chunks=120),
+    "tiny-fp32": dict(heads=2, head_dim=64, tokens_per_block=64, frames=1, budget=8, layers=1, dtype="f32",
+                      chunks=40),
 }
 
 HBM_PEAK_GBS = 8000.0
@@ -57,7 +63,8 @@ def attn_traffic(workload):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=112)
+    p.add_argument("--steps", type=int, default=None,
+                   help="timed chunks (default: the workload's chunk count minus the warm-up)")
     p.add_argument("--warmup", type=int, default=8)
     p.add_argument("--workload", default="wan1.3b-1layer", choices=sorted(WORKLOADS))
     p.add_argument("--beta", type=float, default=0.3)
@@ -119,6 +126,8 @@ def main():
     tdtype = torch.bfloat16 if wl["dtype"] == "bf16" else torch.float32
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.steps is None:
+        args.steps = wl["chunks"] - args.warmup
     chunks = args.warmup + args.steps
 
     # ---- inputs, resident in HBM before timing -------------------------------
@@ -174,28 +183,37 @@ def main():
     for c in range(args.warmup):
         chunk_step(c)
     torch.cuda.synchronize()
-    merges_before, _ = cache.merge_log(cap=0)
+    merges_before, anchor_before = cache.merge_counts()
 
     # ---- timed region: whole chunk steps, with events around every call on
     # the stream the kernels run on (per-kernel averages come from these) -----
     t_start, t_end = new_pair()
     ev = {"attn": [], "ins": [], "cons": []}
+    marks = []
     torch.cuda.synchronize()
     t_start.record(stream)
+    t_prog = time.time()
     for c in range(args.warmup, chunks):
+        marks.append(torch.cuda.Event(enable_timing=True))
+        marks[-1].record(stream)
         chunk_step(c, ev)
+        if time.time() - t_prog > 30:
+            print(f"bench: chunk {c + 1}/{chunks} enqueued", file=sys.stderr, flush=True)
+            t_prog = time.time()
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_chunk = ms_total / args.steps
+    marks.append(t_end)
+    per_chunk = sorted(a.elapsed_time(b) for a, b in zip(marks[:-1], marks[1:]))
+    ms_median = per_chunk[len(per_chunk) // 2]
     attn_ms = [a.elapsed_time(b) for a, b in ev["attn"]]
     ins_ms = [a.elapsed_time(b) for a, b in ev["ins"]]
     cons_ms = [a.elapsed_time(b) for a, b in ev["cons"]]
     cache_timed = cache
 
-    total_merges, log = cache_timed.merge_log(cap=4096)
-    timed_log = log[len(log) - (total_merges - merges_before):] if total_merges > merges_before else []
-    weighted = sum(1 for j in timed_log if not (anchor and j == 0))
+    total_merges, anchor_total = cache_timed.merge_counts()
+    weighted = (total_merges - merges_before) - (anchor_total - anchor_before)
     blk = frame_elems * elt
     lk = M * N + F * N                      # keys per attention call at steady state
     attn_flop = 4.0 * (F * N) * lk * D * H  # QK^T and PV, per layer-call
@@ -220,6 +238,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_chunk, 4),
+        "ms_per_chunk_median": round(ms_median, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,

@@ -17,8 +17,8 @@
  *   Element type is fp32 or bf16 as configured (dtype); LSE is fp32.
  * - Device pointers must be 16-byte aligned; the pool 256-byte aligned.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *   Every call except fademem_get_state, fademem_entry_kv and
- *   fademem_merge_log is asynchronous on that stream and never waits for
+ *   Every call except fademem_get_state, fademem_entry_kv,
+ *   fademem_merge_log and fademem_merge_counts is asynchronous on that stream and never waits for
  *   the device.  One cache is used by one host thread and one stream at a
  *   time.
  * - Ownership: the caller allocates and owns the device pool and every
@@ -168,6 +168,13 @@ int fademem_entry_kv(fademem_cache* cache, int32_t layer, int64_t i, const void*
  * are copied into j[].  Synchronises `stream`. */
 int fademem_merge_log(fademem_cache* cache, int32_t* j, int64_t cap, int64_t* total,
                       void* stream);
+
+/* Counts of the consolidations run so far (Algorithm S1's merge step):
+ * *total of them, *anchor of which merged the anchor's pair (no K/V work),
+ * so total - anchor merges moved K/V bytes.  Either pointer may be NULL.
+ * Unlike the log these counts are not capped.  Synchronises `stream`.
+ * Errors: EINVAL (NULL cache), EHIP. */
+int fademem_merge_counts(fademem_cache* cache, int64_t* total, int64_t* anchor, void* stream);
 
 /* hipError_t value of the last FADEMEM_EHIP on this cache (0 if none). */
 int fademem_last_hip_error(const fademem_cache* cache);

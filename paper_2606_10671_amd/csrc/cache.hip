@@ -626,4 +626,16 @@ int fademem_merge_log(fademem_cache* c, int32_t* j, int64_t cap, int64_t* total,
   return FADEMEM_OK;
 }
 
+int fademem_merge_counts(fademem_cache* c, int64_t* total, int64_t* anchor, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  DevHeader h;
+  e = hipMemcpy(&h, c->pool, sizeof(h), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(c, e);
+  if (total) *total = h.merges_total;
+  if (anchor) *anchor = h.anchor_merges;
+  return FADEMEM_OK;
+}
+
 }  // extern "C"

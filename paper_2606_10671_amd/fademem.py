@@ -32,7 +32,8 @@ MERGE_OPS = {"sqrt_span": FADEMEM_MERGE_SQRT_SPAN, "average": FADEMEM_MERGE_AVER
 EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
     "fademem_consolidate", "fademem_attend", "fademem_count", "fademem_get_state",
-    "fademem_entry_kv", "fademem_merge_log", "fademem_last_hip_error", "fademem_strerror",
+    "fademem_entry_kv", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
+    "fademem_strerror",
 )
 
 
@@ -98,6 +99,7 @@ def lib() -> ctypes.CDLL:
                                     c_void_p]
     L.fademem_entry_kv.argtypes = [c_void_p, c_int32, c_int64, P(c_void_p), P(c_void_p), c_void_p]
     L.fademem_merge_log.argtypes = [c_void_p, P(c_int32), c_int64, P(c_int64), c_void_p]
+    L.fademem_merge_counts.argtypes = [c_void_p, P(c_int64), P(c_int64), c_void_p]
     L.fademem_last_hip_error.argtypes = [c_void_p]
     for name in EXPORTED:
         if name != "fademem_strerror":
@@ -191,6 +193,14 @@ def fademem_merge_log(handle: int, cap: int = 4096, stream: int = 0):
     return total.value, list(buf[:keep])
 
 
+def fademem_merge_counts(handle: int, stream: int = 0):
+    """(total consolidations run, anchor merges among them)."""
+    total, anchor = ctypes.c_int64(0), ctypes.c_int64(0)
+    _ok(lib().fademem_merge_counts(ctypes.c_void_p(handle), ctypes.byref(total), ctypes.byref(anchor),
+                                   ctypes.c_void_p(stream)), "fademem_merge_counts")
+    return total.value, anchor.value
+
+
 def fademem_last_hip_error(handle: int) -> int:
     return lib().fademem_last_hip_error(ctypes.c_void_p(handle))
 
@@ -277,6 +287,9 @@ class Cache:
 
     def merge_log(self, cap: int = 4096, stream=None):
         return fademem_merge_log(self.handle, cap, self._stream(stream))
+
+    def merge_counts(self, stream=None):
+        return fademem_merge_counts(self.handle, self._stream(stream))
 
     def entry_kv(self, layer: int, i: int, stream=None):
         """Views of logical entry i's K and V (valid until the next update)."""

@@ -67,6 +67,7 @@ def run_fullsize(H, D, N, F, M, chunks, layers=1, heads=(0,), check_layers=(0,),
     total, log = cache.merge_log()
     oc0 = next(iter(ocs.values()))
     assert total == len(oc0.merge_log) and log == oc0.merge_log[-len(log):]
+    assert cache.merge_counts() == (len(oc0.merge_log), oc0.anchor_merges)
     print(f"worst max-abs {worst[0]:.3e} normwise {worst[1]:.3e} lse {worst[2]:.3e}", flush=True)
     return cache, oc0
 
