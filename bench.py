@@ -71,10 +71,42 @@ def parse():
     p.add_argument("--no-anchor", action="store_true")
     p.add_argument("--merge-op", default="sqrt_span", choices=["sqrt_span", "average", "select_nearest", "max"],
                    help="consolidation operator (Sec. 3.3 default, or a Table 4 ablation)")
+    p.add_argument("--update", default="fused", choices=["fused", "single"],
+                   help="fused: one fademem_update per chunk (the F updates in one pass); single: "
+                        "fademem_insert + fademem_consolidate per frame")
+    p.add_argument("--denoise-steps", type=int, default=1,
+                   help="attention calls per layer per chunk (the generator's sampler calls it once per denoising "
+                        "step on the same memory; the update follows the last step)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
+
+
+def fused_block_ios(js, count0, F, M, anchor, merge_op):
+    """K (or V) block loads and stores of one fused chunk update, replayed
+    from the merge decisions the library logged for it (no schedule
+    arithmetic here): an operand is loaded once unless it is the result of
+    an earlier merge of the same update; every new or changed entry is
+    stored once, and a frame kept as is is also loaded once."""
+    refs = ["old"] * count0
+    loads = 0
+    it = iter(js)
+    for _ in range(F):
+        refs.append("frame")
+        if len(refs) > M:
+            j = next(it)
+            a, b = refs[j], refs[j + 1]
+            if anchor and j == 0:
+                new = a
+            elif merge_op == "select_nearest":
+                new = b
+            else:
+                loads += (a != "res") + (b != "res")
+                new = "res"
+            refs[j:j + 2] = [new]
+    outs = [r for r in refs if r != "old"]
+    return loads + outs.count("frame"), len(outs)
 
 
 def cpu_baseline(wl, head_inputs, beta, anchor, budget_s, merge_op="sqrt_span"):
@@ -157,14 +189,23 @@ def main():
 
     def chunk_step(c, ev=None):
         per_layer = inputs[c % distinct]
-        for l in range(L):
-            q, k, v = per_layer[l]
+        for _ in range(args.denoise_steps):
+            for l in range(L):
+                q, k, v = per_layer[l]
+                if ev is not None:
+                    ev["attn"].append(new_pair())
+                    ev["attn"][-1][0].record(stream)
+                cache.attend(q, k, v, layer=l, out=out)
+                if ev is not None:
+                    ev["attn"][-1][1].record(stream)
+        if ev is not None:
+            ev["upd"].append(new_pair())
+            ev["upd"][-1][0].record(stream)
+        if args.update == "fused":
+            cache.update([per_layer[l][1] for l in range(L)], [per_layer[l][2] for l in range(L)], c * F)
             if ev is not None:
-                ev["attn"].append(new_pair())
-                ev["attn"][-1][0].record(stream)
-            cache.attend(q, k, v, layer=l, out=out)
-            if ev is not None:
-                ev["attn"][-1][1].record(stream)
+                ev["upd"][-1][1].record(stream)
+            return
         for f in range(F):
             ks = [per_layer[l][1][f * N:(f + 1) * N] for l in range(L)]
             vs = [per_layer[l][2][f * N:(f + 1) * N] for l in range(L)]
@@ -179,6 +220,8 @@ def main():
             cache.consolidate()
             if ev is not None:
                 ev["cons"][-1][1].record(stream)
+        if ev is not None:
+            ev["upd"][-1][1].record(stream)
 
     for c in range(args.warmup):
         chunk_step(c)
@@ -188,7 +231,7 @@ def main():
     # ---- timed region: whole chunk steps, with events around every call on
     # the stream the kernels run on (per-kernel averages come from these) -----
     t_start, t_end = new_pair()
-    ev = {"attn": [], "ins": [], "cons": []}
+    ev = {"attn": [], "ins": [], "cons": [], "upd": []}
     marks = []
     torch.cuda.synchronize()
     t_start.record(stream)
@@ -210,6 +253,7 @@ def main():
     attn_ms = [a.elapsed_time(b) for a, b in ev["attn"]]
     ins_ms = [a.elapsed_time(b) for a, b in ev["ins"]]
     cons_ms = [a.elapsed_time(b) for a, b in ev["cons"]]
+    upd_ms = [a.elapsed_time(b) for a, b in ev["upd"]]
     cache_timed = cache
 
     total_merges, anchor_total = cache_timed.merge_counts()
@@ -224,7 +268,34 @@ def main():
     merge_bytes = 0 if args.merge_op == "select_nearest" else weighted * 3 * 2 * blk * L
     cons_s = sum(cons_ms) / 1e3
     merge_gbps = merge_bytes / cons_s / 1e9 if cons_s > 0 and merge_bytes > 0 else None
-    ins_gbps = len(ins_ms) * 2 * 2 * blk * L / (sum(ins_ms) / 1e3) / 1e9
+    ins_gbps = len(ins_ms) * 2 * 2 * blk * L / (sum(ins_ms) / 1e3) / 1e9 if ins_ms else None
+    # Fused updates: algorithmic bytes from the logged merge decisions of the
+    # timed chunks (the trailing chunks whose merges the log still holds).
+    update_gbps = None
+    if args.update == "fused":
+        count, per_chunk_merges, count0s = 0, [], []
+        for c in range(chunks):
+            count0s.append(count)
+            m = 0
+            for _ in range(F):
+                count += 1
+                if count > M:
+                    count -= 1
+                    m += 1
+            per_chunk_merges.append(m)
+        _, log = cache_timed.merge_log(cap=4096)
+        timed = list(range(args.warmup, chunks))
+        while timed and sum(per_chunk_merges[c] for c in timed) > len(log):
+            timed.pop(0)
+        js = log[len(log) - sum(per_chunk_merges[c] for c in timed):]
+        bytes_, pos = 0, 0
+        for c in timed:
+            n = per_chunk_merges[c]
+            loads, stores = fused_block_ios(js[pos:pos + n], count0s[c], F, M, anchor, args.merge_op)
+            pos += n
+            bytes_ += (loads + stores) * 2 * blk * L
+        t_s = sum(upd_ms[c - args.warmup] for c in timed) / 1e3
+        update_gbps = bytes_ / t_s / 1e9 if t_s > 0 and bytes_ > 0 else None
 
     state = cache_timed.state()
     peak_bytes = cache_timed.pool_bytes
@@ -247,15 +318,23 @@ def main():
         "config": {"workload": args.workload, "heads": H, "head_dim": D, "tokens_per_block": N,
                    "frames_per_chunk": F, "query_tokens": F * N, "budget": M, "beta": args.beta,
                    "anchor": anchor, "merge_op": args.merge_op, "layers": L, "chunks": chunks,
+                   "update": args.update, "denoise_steps": args.denoise_steps,
                    "keys_per_attend": lk},
         "attention_tflops": round(attn_tflops, 2),
         "attention_ms_per_call": round(attn_avg_s * 1e3, 4),
+        "update": args.update,
+        "denoise_steps": args.denoise_steps,
+        "update_ms_per_chunk": round(sum(upd_ms) / len(upd_ms), 4),
+        "update_gbps": round(update_gbps, 1) if update_gbps else None,
+        "update_note": ("fused: algorithmic bytes of one pass (each operand block loaded once, each changed "
+                        "entry stored once) / time of the update call (plan + data kernels)"
+                        if args.update == "fused" else "single: F x (insert + consolidate) per chunk"),
         "merge_gbps": round(merge_gbps, 1) if merge_gbps else None,
-        "merge_note": "algorithmic bytes of weighted merges / time of consolidate calls (schedule + merge kernels)",
+        "merge_note": "single-frame path only: algorithmic bytes of weighted merges / time of consolidate calls",
         "weighted_merges_timed": weighted,
-        "consolidate_ms_per_call": round(cons_s * 1e3 / max(len(cons_ms), 1), 4),
-        "insert_gbps": round(ins_gbps, 1),
-        "insert_ms_per_call": round(sum(ins_ms) / len(ins_ms), 4),
+        "consolidate_ms_per_call": round(cons_s * 1e3 / len(cons_ms), 4) if cons_ms else None,
+        "insert_gbps": round(ins_gbps, 1) if ins_gbps else None,
+        "insert_ms_per_call": round(sum(ins_ms) / len(ins_ms), 4) if ins_ms else None,
         "pool_bytes": peak_bytes,
         "final_spans": state["span"],
         "roofline": {

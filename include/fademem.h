@@ -134,6 +134,24 @@ int fademem_insert(fademem_cache* cache, const void* const* k, const void* const
  * never crosses to the host.  Errors: EHIP. */
 int fademem_consolidate(fademem_cache* cache, void* stream);
 
+/* A chunk's F updates in one call: for f = 0..frames-1, append frame f at
+ * position first_position + f, then consolidate when over budget -- the
+ * F sequential Alg. S1 updates that follow a chunk's final denoising step
+ * (Sec. 4.1; supplementary Sec. S4: one entry per latent frame).  State,
+ * merge log and every stored K/V bit equal those of `frames` calls of
+ * fademem_insert + fademem_consolidate.  Each K/V block that changes is
+ * written once (a chain of merges is evaluated in registers, each merge
+ * rounded to the storage type as on its own), and frames that a merge of
+ * the same call consumes are read from the caller's buffers, never copied
+ * into the pool.  k[l], v[l] (host arrays of `layers` device pointers) are
+ * layer l's chunk, [frames*N][H][D], frame f in rows f*N..(f+1)*N-1; the
+ * caller may reuse them once the stream has passed the call.
+ * Errors: EINVAL (NULL/misaligned pointers, frames < 1, positions out of
+ * range), ESTATE (first_position not above the newest position, or M+1
+ * entries held), EHIP. */
+int fademem_update(fademem_cache* cache, const void* const* k, const void* const* v, int64_t frames,
+                   int64_t first_position, void* stream);
+
 /* Attention of the chunk's queries over layer `layer`'s exposed cache:
  * O_h = softmax(scale * Q_h K_h^T) V_h per head, with the keys/values
  * [memory entries in memory order || current chunk] (Sec. 3.1, Sec. 4.1),

@@ -7,6 +7,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "fademem_internal.h"
@@ -157,6 +158,86 @@ __device__ __forceinline__ uint32_t pack_bf16_rne(double lo, double hi) {
 __device__ __forceinline__ double bf16_lo(uint32_t w) { return double(__uint_as_float(w << 16)); }
 __device__ __forceinline__ double bf16_hi(uint32_t w) { return double(__uint_as_float(w & 0xffff0000u)); }
 
+// The schedule of one consolidation (Sec. 3.3 "Distance-aware scheduling",
+// Alg. S1) over entries 0..n-1 (the newest is n-1), for a 256-thread block:
+//   d_i = t - mu_i = (t*s_i - pos_sum_i) / s_i   (exact numerator, one fp64 division)
+//   u_i = d_i^beta
+//   g_i = |u_{i+1} - u_i| for the pairs i = 0..n-3 (the pair holding the
+//         newest entry, n-2..n-1, is not eligible)
+//   j   = lowest i with g_i - min(g) <= 1e-9 * min(g)
+// Every thread returns j.  span/pos_sum may live in global or LDS memory.
+__device__ int select_pair(const int64_t* span, const int64_t* pos_sum, int n, int64_t t, double beta,
+                           double* u_s, double* g_s, double* red_d, int* red_i) {
+#pragma clang fp contract(off)
+  const int tid = threadIdx.x;
+  for (int i = tid; i < n - 1; i += 256) {
+    const int64_t s = span[i];
+    const double d = double(t * s - pos_sum[i]) / double(s);
+    u_s[i] = (beta == 1.0) ? d : pow(d, beta);
+  }
+  __syncthreads();
+  double gmin = INFINITY;
+  for (int i = tid; i < n - 2; i += 256) {
+    const double g = fabs(u_s[i + 1] - u_s[i]);
+    g_s[i] = g;
+    gmin = fmin(gmin, g);
+  }
+  const double gm = block_min_f64(gmin, red_d);
+  const double tol = 1e-9 * gm;
+  int cand = 0x7fffffff;
+  for (int i = tid; i < n - 2; i += 256) {
+    if (g_s[i] - gm <= tol) cand = min(cand, i);
+  }
+  return block_min_i32(cand, red_i);
+}
+
+// One 16-byte unit of a merge: x is the older entry's, y the newer entry's.
+// Weighted (and average): each element w_a*x + w_b*y in fp64 (two products,
+// one sum) rounded once to the storage type; max pooling: the newer value
+// only when strictly greater.
+template <bool BF16, bool MAXOP>
+__device__ __forceinline__ u32x4 merge_unit(u32x4 x, u32x4 y, double wa, double wb) {
+#pragma clang fp contract(off)
+  u32x4 o;
+  if constexpr (MAXOP) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if constexpr (BF16) {
+        const uint32_t xl = x[w] << 16, yl = y[w] << 16;
+        const uint32_t xh = x[w] & 0xFFFF0000u, yh = y[w] & 0xFFFF0000u;
+        const uint32_t lo = (__uint_as_float(yl) > __uint_as_float(xl)) ? yl : xl;
+        const uint32_t hi = (__uint_as_float(yh) > __uint_as_float(xh)) ? yh : xh;
+        o[w] = (lo >> 16) | hi;
+      } else {
+        o[w] = (__uint_as_float(y[w]) > __uint_as_float(x[w])) ? y[w] : x[w];
+      }
+    }
+  } else if constexpr (BF16) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const double lo = wa * bf16_lo(x[w]) + wb * bf16_lo(y[w]);
+      const double hi = wa * bf16_hi(x[w]) + wb * bf16_hi(y[w]);
+      o[w] = pack_bf16_rne(lo, hi);
+    }
+  } else {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const double v = wa * double(__uint_as_float(x[w])) + wb * double(__uint_as_float(y[w]));
+      o[w] = __float_as_uint(float(v));
+    }
+  }
+  return o;
+}
+
+// Weights (w_j, w_j+1) of a merge of spans s_j, s_j+1 under `op`.
+__device__ __forceinline__ void merge_weights(int op, int64_t s_j, int64_t s_j1, double* wa, double* wb) {
+#pragma clang fp contract(off)
+  const double rj = sqrt(double(s_j));
+  const double rj1 = sqrt(double(s_j1));
+  *wa = op == FADEMEM_MERGE_AVERAGE ? 0.5 : rj / (rj + rj1);
+  *wb = 1.0 - *wa;
+}
+
 struct ConsolidateArgs {
   char* pool;
   Layout lay;
@@ -172,13 +253,8 @@ struct ConsolidateArgs {
 
 // One consolidation (Sec. 3.3 "Distance-aware scheduling" and
 // "Consolidation operator", Alg. S1) in one launch.  Every block derives
-// the decision from the current metadata copy, which no block writes:
-//   d_i = t - mu_i = (t*s_i - pos_sum_i) / s_i   (exact numerator, one fp64 division)
-//   u_i = d_i^beta
-//   g_i = |u_{i+1} - u_i| for the pairs i = 0..n-3 (the pair holding the
-//         newest entry, n-2..n-1, is not eligible)
-//   j   = lowest i with g_i - min(g) <= 1e-9 * min(g)
-// Block 0 writes the spliced metadata into the other copy (spans add,
+// the decision (select_pair) from the current metadata copy, which no block
+// writes.  Block 0 writes the spliced metadata into the other copy (spans add,
 // pos_sum adds so mu is span-weighted; the anchor keeps its position, the
 // slot of entry j+1 is freed) and appends j to the merge log.  Unless the
 // pair holds the anchor, all blocks then merge entry j+1 into entry j's
@@ -197,25 +273,7 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
   const Meta m = meta_of(a.pool, a.lay, a.cur);
   const int n = a.n;
   const int tid = threadIdx.x;
-  for (int i = tid; i < n - 1; i += 256) {
-    const int64_t s = m.span[i];
-    const double d = double(a.t * s - m.pos_sum[i]) / double(s);
-    u_s[i] = (a.beta == 1.0) ? d : pow(d, a.beta);
-  }
-  __syncthreads();
-  double gmin = INFINITY;
-  for (int i = tid; i < n - 2; i += 256) {
-    const double g = fabs(u_s[i + 1] - u_s[i]);
-    g_s[i] = g;
-    gmin = fmin(gmin, g);
-  }
-  const double gm = block_min_f64(gmin, red_d);
-  const double tol = 1e-9 * gm;
-  int cand = 0x7fffffff;
-  for (int i = tid; i < n - 2; i += 256) {
-    if (g_s[i] - gm <= tol) cand = min(cand, i);
-  }
-  const int j = block_min_i32(cand, red_i);
+  const int j = select_pair(m.span, m.pos_sum, n, a.t, a.beta, u_s, g_s, red_d, red_i);
 
   const int64_t s_j = m.span[j], s_j1 = m.span[j + 1];
   const bool anchor_pair = a.anchor && j == 0;
@@ -263,10 +321,8 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
   }
   if (anchor_pair || select) return;  // the anchor keeps its K and V; selection moves nothing
 
-  const double rj = sqrt(double(s_j));
-  const double rj1 = sqrt(double(s_j1));
-  const double wa = a.op == FADEMEM_MERGE_AVERAGE ? 0.5 : rj / (rj + rj1);
-  const double wb = 1.0 - wa;
+  double wa, wb;
+  merge_weights(a.op, s_j, s_j1, &wa, &wb);
   const int64_t step = int64_t(gridDim.x) * 256 * UNROLL;
   {
     const int plane = blockIdx.y;  // layer * 2 + kv
@@ -287,40 +343,256 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
       for (int r = 0; r < UNROLL; ++r) {
         const int64_t u = base + int64_t(r) * 256;
         if (u < a.units) {
-          u32x4 o;
-          if constexpr (MAXOP) {
-            // Max pooling: the newer value (y) only when strictly greater,
-            // so equal values keep the older bits.
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              if constexpr (BF16) {
-                const uint32_t xl = x[r][w] << 16, yl = y[r][w] << 16;
-                const uint32_t xh = x[r][w] & 0xFFFF0000u, yh = y[r][w] & 0xFFFF0000u;
-                const uint32_t lo = (__uint_as_float(yl) > __uint_as_float(xl)) ? yl : xl;
-                const uint32_t hi = (__uint_as_float(yh) > __uint_as_float(xh)) ? yh : xh;
-                o[w] = (lo >> 16) | hi;
-              } else {
-                o[w] = (__uint_as_float(y[r][w]) > __uint_as_float(x[r][w])) ? y[r][w] : x[r][w];
-              }
-            }
-          } else if constexpr (BF16) {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              const double lo = wa * bf16_lo(x[r][w]) + wb * bf16_lo(y[r][w]);
-              const double hi = wa * bf16_hi(x[r][w]) + wb * bf16_hi(y[r][w]);
-              o[w] = pack_bf16_rne(lo, hi);
-            }
-          } else {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-              const double v = wa * double(__uint_as_float(x[r][w])) + wb * double(__uint_as_float(y[r][w]));
-              o[w] = __float_as_uint(float(v));
-            }
-          }
+          const u32x4 o = merge_unit<BF16, MAXOP>(x[r], y[r], wa, wb);
           __builtin_nontemporal_store(o, dst + u);
         }
       }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fused update: F sequential Algorithm S1 updates (append frame f, then
+// consolidate if over budget) in two launches.  The plan kernel replays the
+// F steps on the metadata with the same schedule arithmetic as
+// consolidate_kernel and records, for every merge that computes K and V,
+// its operands (an old entry's slot, a frame of the caller's chunk, or an
+// earlier merge of this update) and weights, and for every entry that ends
+// up new or changed, where it comes from and the slot it goes to.  The data
+// kernel then streams each (layer, K|V) plane once: per 16-byte unit it
+// loads each operand once, evaluates the merges in order in registers
+// (each rounded to the storage type exactly as a lone merge is), and stores
+// each changed entry once.  Frames consumed by a merge of the same update
+// are read from the caller's buffers and never copied into the pool.
+// ---------------------------------------------------------------------------
+
+struct PlanArgs {
+  char* pool;
+  Layout lay;
+  int n0;                  // entries held before the update (<= M)
+  int frames;              // 1..kMaxPlanFrames
+  int64_t first_position;  // position of frame 0; frame f is first_position + f
+  int64_t budget;          // M
+  double beta;
+  int anchor;
+  int op;
+  int cur;                 // metadata copy read; the other copy is written
+};
+
+__global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
+#pragma clang fp contract(off)
+  constexpr int kCap = kMaxBudget + 1;  // entries held at most (M + 1)
+  __shared__ int64_t first_s[kCap], pos_s[kCap], span_s[kCap];
+  __shared__ int32_t kind_s[kCap], idx_s[kCap];
+  __shared__ int32_t free_s[kCap];
+  __shared__ double u_s[kCap], g_s[kCap];
+  __shared__ double red_d[4];
+  __shared__ int red_i[4];
+  __shared__ int n_free_s;
+  __shared__ UpdatePlan plan;
+
+  const int tid = threadIdx.x;
+  const Meta m = meta_of(a.pool, a.lay, a.cur);
+  const int slots = int(a.lay.slots);
+  for (int i = tid; i < a.n0; i += 256) {
+    first_s[i] = m.first[i];
+    pos_s[i] = m.pos_sum[i];
+    span_s[i] = m.span[i];
+    kind_s[i] = kRefSlot;
+    idx_s[i] = m.order[i];
+  }
+  for (int i = a.n0 + tid; i < slots; i += 256) free_s[i - a.n0] = m.order[i];
+  if (tid == 0) {
+    n_free_s = slots - a.n0;
+    plan.n_ar = 0;
+    plan.n_out = 0;
+  }
+  __syncthreads();
+
+  DevHeader* hdr = reinterpret_cast<DevHeader*>(a.pool);
+  int32_t* log = reinterpret_cast<int32_t*>(a.pool + a.lay.off_log);
+  int n = a.n0;
+  for (int f = 0; f < a.frames; ++f) {
+    const int64_t t = a.first_position + f;
+    if (tid == 0) {  // Append (K_t, V_t, t, 1), its K, V still the caller's frame f
+      first_s[n] = t;
+      pos_s[n] = t;
+      span_s[n] = 1;
+      kind_s[n] = kRefFrame;
+      idx_s[n] = f;
+    }
+    n += 1;
+    __syncthreads();
+    if (n <= a.budget) continue;  // within budget: nothing to consolidate (uniform)
+    const int j = select_pair(span_s, pos_s, n, t, a.beta, u_s, g_s, red_d, red_i);
+    if (tid == 0) {
+      const bool anchor_pair = a.anchor && j == 0;
+      const bool select = a.op == FADEMEM_MERGE_SELECT_NEAREST && !anchor_pair;
+      const int64_t s_new = span_s[j] + span_s[j + 1];
+      int32_t nk, ni;  // reference of the merged entry
+      if (anchor_pair || select) {
+        // The kept entry's K, V move unchanged; the other one's are dropped.
+        const int keep = anchor_pair ? j : j + 1, drop = anchor_pair ? j + 1 : j;
+        nk = kind_s[keep];
+        ni = idx_s[keep];
+        if (kind_s[drop] == kRefSlot) free_s[n_free_s++] = idx_s[drop];
+      } else {
+        const int k = plan.n_ar++;
+        plan.a_kind[k] = kind_s[j];
+        plan.a_idx[k] = idx_s[j];
+        plan.b_kind[k] = kind_s[j + 1];
+        plan.b_idx[k] = idx_s[j + 1];
+        merge_weights(a.op, span_s[j], span_s[j + 1], &plan.wa[k], &plan.wb[k]);
+        if (kind_s[j] == kRefSlot) free_s[n_free_s++] = idx_s[j];
+        if (kind_s[j + 1] == kRefSlot) free_s[n_free_s++] = idx_s[j + 1];
+        nk = kRefResult;
+        ni = k;
+      }
+      pos_s[j] = anchor_pair ? first_s[j] * s_new : pos_s[j] + pos_s[j + 1];
+      span_s[j] = s_new;
+      kind_s[j] = nk;
+      idx_s[j] = ni;
+      const int64_t lk = hdr->merges_total;
+      log[lk % kLogCap] = j;
+      hdr->merges_total = lk + 1;
+      if (anchor_pair) hdr->anchor_merges += 1;
+    }
+    __syncthreads();
+    // Replace: entries j+2..n-1 move down by one.
+    constexpr int kPer = (kCap + 255) / 256;
+    int64_t tf[kPer], tp[kPer], ts[kPer];
+    int32_t tk[kPer], ti[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = j + 1 + tid + 256 * r;
+      if (i < n - 1) {
+        tf[r] = first_s[i + 1];
+        tp[r] = pos_s[i + 1];
+        ts[r] = span_s[i + 1];
+        tk[r] = kind_s[i + 1];
+        ti[r] = idx_s[i + 1];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int i = j + 1 + tid + 256 * r;
+      if (i < n - 1) {
+        first_s[i] = tf[r];
+        pos_s[i] = tp[r];
+        span_s[i] = ts[r];
+        kind_s[i] = tk[r];
+        idx_s[i] = ti[r];
+      }
+    }
+    n -= 1;
+    __syncthreads();
+  }
+
+  // Slots: kept old entries stay; every new or changed entry takes a free
+  // slot (those free before, or freed by this update).
+  const Meta w = meta_of(a.pool, a.lay, a.cur ^ 1);
+  if (tid == 0) {
+    int next = 0;
+    for (int i = 0; i < n; ++i) {
+      if (kind_s[i] == kRefSlot) {
+        w.order[i] = idx_s[i];
+      } else {
+        const int o = plan.n_out++;
+        const int32_t slot = free_s[next++];
+        plan.o_kind[o] = kind_s[i];
+        plan.o_idx[o] = idx_s[i];
+        plan.o_slot[o] = slot;
+        w.order[i] = slot;
+      }
+    }
+    for (int i = n; i < slots; ++i) w.order[i] = free_s[next++];
+    *reinterpret_cast<UpdatePlan*>(a.pool + a.lay.off_prog) = plan;
+  }
+  for (int i = tid; i < n; i += 256) {
+    w.first[i] = first_s[i];
+    w.pos_sum[i] = pos_s[i];
+    w.span[i] = span_s[i];
+  }
+}
+
+struct UpdateDataArgs {
+  const void* k[kMaxLayersPerLaunch];  // layer's chunk K, [frames][N][H][D]
+  const void* v[kMaxLayersPerLaunch];
+  char* pool;
+  Layout lay;
+  int64_t layer0;  // first layer of this launch
+  int64_t units;   // 16-byte units per K (or V) block
+};
+
+template <bool BF16, bool MAXOP>
+__global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
+  constexpr int kM = kMaxPlanFrames, kO = 2 * kMaxPlanFrames;
+  const UpdatePlan* P = reinterpret_cast<const UpdatePlan*>(a.pool + a.lay.off_prog);
+  const int n_ar = P->n_ar, n_out = P->n_out;
+  const int li = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const int64_t layer = a.layer0 + li;
+  const char* chunk = static_cast<const char*>(kv ? a.v[li] : a.k[li]);
+  auto ref = [&](int kind, int idx) -> const u32x4* {
+    return reinterpret_cast<const u32x4*>(kind == kRefSlot ? a.pool + kv_offset(a.lay, layer, idx, kv)
+                                                           : chunk + size_t(idx) * a.lay.blk_bytes);
+  };
+  const u32x4* pa[kM];
+  const u32x4* pb[kM];
+  int ra[kM], rb[kM];
+  double wa[kM], wb[kM];
+#pragma unroll
+  for (int k = 0; k < kM; ++k) {
+    const bool on = k < n_ar;
+    ra[k] = on && P->a_kind[k] == kRefResult ? P->a_idx[k] : -1;
+    rb[k] = on && P->b_kind[k] == kRefResult ? P->b_idx[k] : -1;
+    pa[k] = on && ra[k] < 0 ? ref(P->a_kind[k], P->a_idx[k]) : nullptr;
+    pb[k] = on && rb[k] < 0 ? ref(P->b_kind[k], P->b_idx[k]) : nullptr;
+    wa[k] = on ? P->wa[k] : 0.0;
+    wb[k] = on ? P->wb[k] : 0.0;
+  }
+  u32x4* po[kO];
+  const u32x4* ps[kO];
+  int ro[kO];
+#pragma unroll
+  for (int o = 0; o < kO; ++o) {
+    const bool on = o < n_out;
+    ro[o] = on && P->o_kind[o] == kRefResult ? P->o_idx[o] : -1;
+    ps[o] = on && ro[o] < 0 ? ref(P->o_kind[o], P->o_idx[o]) : nullptr;
+    po[o] = on ? reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, layer, P->o_slot[o], kv)) : nullptr;
+  }
+  // Result r of the merges computed so far (r is wave-uniform).
+  auto pick = [](const u32x4 (&R)[kM], int r) {
+    u32x4 x = R[0];
+#pragma unroll
+    for (int k = 1; k < kM; ++k)
+      if (r == k) x = R[k];
+    return x;
+  };
+  const int64_t stride = int64_t(gridDim.x) * 256;
+  for (int64_t u = int64_t(blockIdx.x) * 256 + threadIdx.x; u < a.units; u += stride) {
+    // Every operand of this unit is loaded before any store (stores may go
+    // to a slot an operand was read from).
+    u32x4 A[kM], B[kM], S[kO], R[kM];
+#pragma unroll
+    for (int k = 0; k < kM; ++k) {
+      if (pa[k]) A[k] = __builtin_nontemporal_load(pa[k] + u);
+      if (pb[k]) B[k] = __builtin_nontemporal_load(pb[k] + u);
+    }
+#pragma unroll
+    for (int o = 0; o < kO; ++o)
+      if (ps[o]) S[o] = __builtin_nontemporal_load(ps[o] + u);
+#pragma unroll
+    for (int k = 0; k < kM; ++k) {
+      if (k < n_ar) {
+        const u32x4 x = pa[k] ? A[k] : pick(R, ra[k]);
+        const u32x4 y = pb[k] ? B[k] : pick(R, rb[k]);
+        R[k] = merge_unit<BF16, MAXOP>(x, y, wa[k], wb[k]);
+      }
+    }
+#pragma unroll
+    for (int o = 0; o < kO; ++o)
+      if (po[o]) __builtin_nontemporal_store(ps[o] ? S[o] : pick(R, ro[o]), po[o] + u);
   }
 }
 
@@ -334,6 +606,40 @@ unsigned plane_blocks(int64_t units, int per_thread) {
   if (b < 1) b = 1;
   if (b > 65535) b = 65535;
   return unsigned(b);
+}
+
+// Blocks of `threads` threads that are resident on the whole device at once
+// for `kernel` (0 on error).  Streaming passes launch one such round, so no
+// block waits for a second round while most CUs idle.
+int resident_blocks(const void* kernel, int threads) {
+  // Cached per (device, kernel, threads): the answer never changes.
+  struct Entry { int dev; const void* kernel; int threads; int blocks; };
+  static Entry seen[32];
+  static int n_seen = 0;
+  static std::mutex mu;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < n_seen; ++i)
+    if (seen[i].dev == dev && seen[i].kernel == kernel && seen[i].threads == threads) return seen[i].blocks;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess) return 0;
+  if (n_seen < 32) seen[n_seen++] = Entry{dev, kernel, threads, cus * per_cu};
+  return cus * per_cu;
+}
+
+// Blocks per plane for a streaming pass over `planes` planes of `units`
+// 16-byte units: one resident round spread over the planes (at least one
+// block per plane), but no more than covering each plane with `per_thread`
+// units per thread.
+unsigned stream_blocks_per_plane(const void* kernel, unsigned planes, int64_t units, int per_thread) {
+  int resident = resident_blocks(kernel, 256);
+  if (resident <= 0) resident = 2048;
+  unsigned per_plane = unsigned(resident) / planes;
+  if (per_plane < 1) per_plane = 1;
+  const unsigned cover = plane_blocks(units, per_thread);
+  return per_plane < cover ? per_plane : cover;
 }
 
 bool valid_config(const fademem_config* c) {
@@ -366,6 +672,7 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
     L.off_order[c] = off;   off = round_up(off + 4 * size_t(L.slots), 256);
   }
   L.off_log = off;     off = round_up(off + 4 * size_t(kLogCap), 256);
+  L.off_prog = off;    off = round_up(off + sizeof(UpdatePlan), 256);
   L.meta_bytes = off;
   L.elt = cfg->dtype == FADEMEM_BF16 ? 2 : 4;
   L.row_elems = size_t(cfg->heads) * size_t(cfg->head_dim);
@@ -513,23 +820,92 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   a.op = c->cfg.merge_op;
   a.cur = c->cur;
   a.units = int64_t(c->lay.blk_bytes / 16);
-  // Blocks per plane: enough to cover it with UNROLL units per thread, but
-  // about 2048 blocks in total (8 per CU) so that every block has work and
-  // the per-block schedule evaluation stays a small fraction of the pass.
-  const unsigned planes = unsigned(2 * c->cfg.layers);
-  unsigned per_plane = 2048u / planes;
-  if (per_plane < 1) per_plane = 1;
-  const unsigned cover = plane_blocks(a.units, kMergeUnroll);
-  if (per_plane > cover) per_plane = cover;
-  const dim3 blocks(per_plane, planes);
   const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
   auto kernel = bf16 ? (maxop ? consolidate_kernel<true, kMergeUnroll, true> : consolidate_kernel<true, kMergeUnroll, false>)
                      : (maxop ? consolidate_kernel<false, kMergeUnroll, true> : consolidate_kernel<false, kMergeUnroll, false>);
+  // One resident round of blocks over the planes (every block also derives
+  // the schedule, so no more blocks than the device holds at once).
+  const unsigned planes = unsigned(2 * c->cfg.layers);
+  const dim3 blocks(stream_blocks_per_plane(reinterpret_cast<const void*>(kernel), planes, a.units, kMergeUnroll),
+                    planes);
   hipLaunchKernelGGL(kernel, dim3(blocks), dim3(256), 0, as_stream(stream), a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(c, e);
   c->cur ^= 1;
   c->count -= 1;
+  return FADEMEM_OK;
+}
+
+int fademem_update(fademem_cache* c, const void* const* k, const void* const* v, int64_t frames,
+                   int64_t first_position, void* stream) {
+  if (!c || !k || !v) return FADEMEM_EINVAL;
+  if (frames < 1 || frames > kMaxTokens) return FADEMEM_EINVAL;
+  // Every position f, first_position <= f <= first_position + frames - 1, must satisfy |f| < 2^40.
+  if (first_position <= -kMaxPosition || first_position > kMaxPosition - frames) return FADEMEM_EINVAL;
+  const int layers = c->cfg.layers;
+  for (int l = 0; l < layers; ++l) {
+    if (!k[l] || !v[l] || !aligned(k[l], 16) || !aligned(v[l], 16)) return FADEMEM_EINVAL;
+  }
+  if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
+  if (c->any_inserted && first_position <= c->newest) return FADEMEM_ESTATE;
+  // t*s_i and first*s_i must stay exact in int64 (as for fademem_insert).
+  {
+    const int64_t last = first_position + frames - 1;
+    const int64_t a0 = first_position < 0 ? -first_position : first_position;
+    const int64_t a1 = last < 0 ? -last : last;
+    const unsigned __int128 mag = (unsigned __int128)(a0 > a1 ? a0 : a1) + 1;
+    if (mag * (unsigned __int128)(c->inserted + frames) >= ((unsigned __int128)1 << 62)) return FADEMEM_ESTATE;
+  }
+  (void)hipGetLastError();
+  const int64_t units = int64_t(c->lay.blk_bytes / 16);
+  const unsigned planes_max = unsigned(2 * (layers < kMaxLayersPerLaunch ? layers : kMaxLayersPerLaunch));
+  const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
+  auto data_kernel = bf16 ? (maxop ? update_data_kernel<true, true> : update_data_kernel<true, false>)
+                          : (maxop ? update_data_kernel<false, true> : update_data_kernel<false, false>);
+  const unsigned per_plane = stream_blocks_per_plane(reinterpret_cast<const void*>(data_kernel), planes_max, units, 1);
+  for (int64_t f0 = 0; f0 < frames; f0 += kMaxPlanFrames) {
+    const int nf = int((frames - f0) < kMaxPlanFrames ? (frames - f0) : kMaxPlanFrames);
+    PlanArgs pa;
+    pa.pool = c->pool;
+    pa.lay = c->lay;
+    pa.n0 = int(c->count);
+    pa.frames = nf;
+    pa.first_position = first_position + f0;
+    pa.budget = c->cfg.budget;
+    pa.beta = c->cfg.beta;
+    pa.anchor = c->cfg.anchor;
+    pa.op = c->cfg.merge_op;
+    pa.cur = c->cur;
+    hipLaunchKernelGGL(update_plan_kernel, dim3(1), dim3(256), 0, as_stream(stream), pa);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(c, e);
+    for (int l0 = 0; l0 < layers; l0 += kMaxLayersPerLaunch) {
+      const int nl = (layers - l0) < kMaxLayersPerLaunch ? (layers - l0) : kMaxLayersPerLaunch;
+      UpdateDataArgs da;
+      memset(&da, 0, sizeof(da));
+      for (int l = 0; l < nl; ++l) {
+        da.k[l] = static_cast<const char*>(k[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
+        da.v[l] = static_cast<const char*>(v[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
+      }
+      da.pool = c->pool;
+      da.lay = c->lay;
+      da.layer0 = l0;
+      da.units = units;
+      hipLaunchKernelGGL(data_kernel, dim3(per_plane, unsigned(2 * nl)), dim3(256), 0, as_stream(stream), da);
+      e = hipGetLastError();
+      if (e != hipSuccess) return hip_fail(c, e);
+    }
+    // Host mirror of the count: each frame appends, then consolidates back
+    // to M when over budget.
+    for (int f = 0; f < nf; ++f) {
+      c->count += 1;
+      if (c->count > c->cfg.budget) c->count -= 1;
+    }
+    c->cur ^= 1;
+    c->inserted += nf;
+    c->newest = first_position + f0 + nf - 1;
+    c->any_inserted = true;
+  }
   return FADEMEM_OK;
 }
 

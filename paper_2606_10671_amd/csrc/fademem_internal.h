@@ -11,12 +11,13 @@
 namespace fademem {
 
 constexpr int kLogCap = 4096;             // merge-log ring capacity (entries)
+constexpr int kMaxPlanFrames = 4;         // frames one fused update plan covers
 constexpr int64_t kMaxBudget = 1023;      // schedule runs in one 1024-thread block
 constexpr int kMaxLayersPerLaunch = 64;   // layer pointers passed as kernel arguments
 constexpr int64_t kMaxPosition = int64_t(1) << 40;
 constexpr int64_t kMaxTokens = int64_t(1) << 30;
 
-// bf16 attention work split.  A workgroup (4 waves x 64 queries) runs one
+// bf16 attention work split.  A workgroup (8 waves x 32 queries) runs one
 // query tile's key range, or part of it: when the tiles do not fill whole
 // rounds of resident workgroups, the remaining tiles are split along the key
 // axis between workgroups, each part leaves its partial result (unnormalised
@@ -42,6 +43,21 @@ struct DevHeader {
   int64_t anchor_merges;  // of which anchor merges (no K/V work)
 };
 
+// Data program of one fused update (F sequential Algorithm S1 updates),
+// written by the plan kernel and executed element by element by the data
+// kernel.  A value reference is an old entry's slot, a frame of the
+// caller's chunk, or the result of an earlier merge of the same update.
+enum : int32_t { kRefSlot = 0, kRefFrame = 1, kRefResult = 2 };
+struct UpdatePlan {
+  int32_t n_ar;                          // merges that compute K, V (in order)
+  int32_t n_out;                         // entries to store
+  int32_t a_kind[kMaxPlanFrames], a_idx[kMaxPlanFrames];  // older operand of merge k
+  int32_t b_kind[kMaxPlanFrames], b_idx[kMaxPlanFrames];  // newer operand of merge k
+  double wa[kMaxPlanFrames], wb[kMaxPlanFrames];          // weights of merge k
+  int32_t o_kind[2 * kMaxPlanFrames], o_idx[2 * kMaxPlanFrames];
+  int32_t o_slot[2 * kMaxPlanFrames];    // destination slot of each stored entry
+};
+
 // Pool layout.  The memory's metadata is kept twice (copies 0 and 1): a
 // consolidation reads the current copy and writes the other one, so the
 // many blocks of the merge kernel that all derive the schedule decision
@@ -56,6 +72,7 @@ struct Layout {
   size_t off_span[2];     // int64[slots]
   size_t off_order[2];    // int32[slots]
   size_t off_log;         // int32[kLogCap]
+  size_t off_prog;        // UpdatePlan of the last fused update
   size_t meta_bytes;      // multiple of 256
   size_t elt;             // bytes per element
   size_t blk_bytes;       // N*H*D*elt: one K (or V) block

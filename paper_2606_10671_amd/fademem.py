@@ -31,7 +31,7 @@ MERGE_OPS = {"sqrt_span": FADEMEM_MERGE_SQRT_SPAN, "average": FADEMEM_MERGE_AVER
 
 EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
-    "fademem_consolidate", "fademem_attend", "fademem_count", "fademem_get_state",
+    "fademem_consolidate", "fademem_update", "fademem_attend", "fademem_count", "fademem_get_state",
     "fademem_entry_kv", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
     "fademem_strerror",
 )
@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
     L.fademem_cache_destroy.argtypes = [c_void_p]
     L.fademem_insert.argtypes = [c_void_p, P(c_void_p), P(c_void_p), c_int64, c_void_p]
     L.fademem_consolidate.argtypes = [c_void_p, c_void_p]
+    L.fademem_update.argtypes = [c_void_p, P(c_void_p), P(c_void_p), c_int64, c_int64, c_void_p]
     L.fademem_attend.argtypes = [c_void_p, c_int32, c_void_p, c_int64, c_void_p, c_void_p, c_int64,
                                  ctypes.c_float, c_void_p, c_void_p, c_void_p]
     L.fademem_count.argtypes = [c_void_p, P(c_int64)]
@@ -150,6 +151,15 @@ def fademem_insert(handle: int, k_ptrs: Sequence[int], v_ptrs: Sequence[int], po
 
 def fademem_consolidate(handle: int, stream: int = 0) -> None:
     _ok(lib().fademem_consolidate(ctypes.c_void_p(handle), ctypes.c_void_p(stream)), "fademem_consolidate")
+
+
+def fademem_update(handle: int, k_ptrs: Sequence[int], v_ptrs: Sequence[int], frames: int, first_position: int,
+                   stream: int = 0) -> None:
+    n = len(k_ptrs)
+    ka = (ctypes.c_void_p * n)(*k_ptrs)
+    va = (ctypes.c_void_p * n)(*v_ptrs)
+    _ok(lib().fademem_update(ctypes.c_void_p(handle), ka, va, frames, first_position, ctypes.c_void_p(stream)),
+        "fademem_update")
 
 
 def fademem_attend(handle: int, layer: int, q_ptr: int, q_tokens: int, k_cur_ptr: int, v_cur_ptr: int,
@@ -262,6 +272,22 @@ class Cache:
 
     def consolidate(self, stream=None):
         fademem_consolidate(self.handle, self._stream(stream))
+
+    def update(self, k, v, first_position: int, stream=None):
+        """A chunk's F updates (insert + consolidate per frame) in one call;
+        k, v: per layer a [F*N][H][D] tensor (or one tensor for one layer)."""
+        ks = k if isinstance(k, (list, tuple)) else [k]
+        vs = v if isinstance(v, (list, tuple)) else [v]
+        if len(ks) != self.cfg.layers or len(vs) != self.cfg.layers:
+            raise ValueError("one K and one V chunk per layer")
+        N = self.cfg.tokens_per_block
+        rows = ks[0].shape[0] if ks[0].dim() == 3 else -1
+        if rows <= 0 or rows % N:
+            raise ValueError(f"chunk rows must be a positive multiple of {N}")
+        for t in list(ks) + list(vs):
+            self._check(t, rows, "chunk")
+        fademem_update(self.handle, [t.data_ptr() for t in ks], [t.data_ptr() for t in vs], rows // N,
+                       first_position, self._stream(stream))
 
     def attend(self, q, k_cur, v_cur, layer: int = 0, scale: float = 0.0, out=None, lse=None, stream=None):
         import torch

@@ -49,7 +49,8 @@ GOOD = dict(budget=21, heads=12, head_dim=128, tokens_per_block=1560, beta=0.3, 
 def test_pool_bytes_layout():
     """Metadata (< 64 KiB) + (M+1) K and V slots per layer; bf16 caches add
     the attention's split-work scratch: two slots per workgroup (at most
-    512) of 128 queries x D fp32 partial O plus 256 fp32 maxima and sums."""
+    256) of 256 queries x D fp32 partial O plus 1024 fp32 maxima and sums
+    (the same bytes as 512 slots of 128 queries x D plus 256 floats)."""
     n = fm.fademem_pool_bytes(fm.make_config(**GOOD))
     blk = 1560 * 12 * 128 * 2
     ws = 2 * 512 * (128 * 128 + 2 * 256) * 4
@@ -95,6 +96,7 @@ def test_null_handles_are_rejected():
     L = fm.lib()
     assert L.fademem_consolidate(None, None) == fm.FADEMEM_EINVAL
     assert L.fademem_insert(None, None, None, 0, None) == fm.FADEMEM_EINVAL
+    assert L.fademem_update(None, None, None, 3, 0, None) == fm.FADEMEM_EINVAL
     assert L.fademem_attend(None, 0, None, 1, None, None, 0, ctypes.c_float(0), None, None, None) == fm.FADEMEM_EINVAL
     n = ctypes.c_int64(0)
     assert L.fademem_count(None, ctypes.byref(n)) == fm.FADEMEM_EINVAL
