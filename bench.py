@@ -77,6 +77,9 @@ def parse():
     p.add_argument("--denoise-steps", type=int, default=1,
                    help="attention calls per layer per chunk (the generator's sampler calls it once per denoising "
                         "step on the same memory; the update follows the last step)")
+    p.add_argument("--rope-pairs", type=int, default=0,
+                   help="temporal RoPE handling: pairs of each head carrying the temporal phase (Wan-class: 22 of "
+                        "64); the memory is exposed re-indexed (0 = off)")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -178,7 +181,7 @@ def main():
         inputs.append(per_layer)
     out = torch.empty((F * N, H, D), dtype=tdtype, device=dev)
     cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=args.beta, anchor=anchor,
-                  dtype=tdtype, layers=L, device=dev, merge_op=args.merge_op)
+                  dtype=tdtype, layers=L, device=dev, merge_op=args.merge_op, rope_pairs=args.rope_pairs)
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -318,7 +321,7 @@ def main():
         "config": {"workload": args.workload, "heads": H, "head_dim": D, "tokens_per_block": N,
                    "frames_per_chunk": F, "query_tokens": F * N, "budget": M, "beta": args.beta,
                    "anchor": anchor, "merge_op": args.merge_op, "layers": L, "chunks": chunks,
-                   "update": args.update, "denoise_steps": args.denoise_steps,
+                   "update": args.update, "denoise_steps": args.denoise_steps, "rope_pairs": args.rope_pairs,
                    "keys_per_attend": lk},
         "attention_tflops": round(attn_tflops, 2),
         "attention_ms_per_call": round(attn_avg_s * 1e3, 4),

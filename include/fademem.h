@@ -89,6 +89,21 @@ typedef struct fademem_config {
   int32_t layers;           /* L >= 1 per-layer memories sharing one schedule.
                                The schedule depends only on positions, so every
                                layer makes the same decisions (Sec. 3.3).       */
+  int32_t rope_pairs;       /* Temporal RoPE handling (Sec. 3.3 "Boundary and
+                               positional handling"): 0 = off (keys are used as
+                               stored).  P > 0: the first P interleaved pairs
+                               (2i, 2i+1) of each head's dimension carry the
+                               temporal rotary phase; 1 <= P <= D/2.  Blocks
+                               are inserted without their temporal phase and
+                               stored so; fademem_attend exposes memory entry
+                               i (0 = oldest) at temporal index i, i.e. pair k
+                               of its keys rotated by the angle i * w_k with
+                               w_k = rope_theta^(-k/P), evaluated in fp64 and
+                               rounded once to the storage type.  The caller
+                               applies the same rotation to the current
+                               chunk's queries and keys at indices n + f (n =
+                               entries held, f = frame within the chunk).    */
+  double  rope_theta;       /* rotary base (> 1), e.g. 10000; ignored if P = 0 */
 } fademem_config;
 
 typedef struct fademem_cache fademem_cache; /* opaque host object */

@@ -12,6 +12,9 @@ from .fademem_oracle import (  # noqa: F401
     bf16_bits,
     bf16_from_bits,
     chunk_step,
+    exposed_kv_rope,
     round_to_bf16,
     round_to_f32,
+    rope_angles,
+    rope_rotate,
 )

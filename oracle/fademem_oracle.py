@@ -24,6 +24,11 @@ What it computes (FadeMem, arXiv 2606.10671):
 * Attention -- Sec. 3.1: the chunk's queries attend over the exposed cache
   [memory entries in order || current chunk].  This is textbook softmax
   attention, written out in fp64.
+* Temporal RoPE handling -- Sec. 3.3 "Boundary and positional handling":
+  memory keys are kept without their temporal rotary phase and re-indexed
+  within a bounded temporal range at attention time.  The rotation of one
+  pair of dimensions by an angle is the plane rotation of rotary position
+  embeddings; which index each retained entry gets is a reading (below).
 
 Readings where the paper is silent (each is listed with its reason in the
 design notes of the repository):
@@ -43,7 +48,14 @@ design notes of the repository):
 * "Select Nearest" keeps the newer entry's K, V (the entry nearer to the
   present, whose distance the schedule measures); max pooling takes, per
   element, the newer entry's value when it is strictly greater, else the
-  older one's (so equal values, including -0 and +0, keep the older bits).
+  older one's (so equal values, including -0 and +0, keep the older bits);
+* temporal RoPE: the first P interleaved pairs (2k, 2k+1) of a head carry
+  the temporal phase, pair k at frequency theta**(-k/P) (the layout of a
+  video model's temporal rotary axis); memory entry i (0 = oldest) is
+  exposed at temporal index i and the current chunk's frame f at n + f
+  (n = entries held).  Parity unpinned as to the paper: the paper does not
+  state the mapping.  The rotation itself is pinned (complex
+  multiplication, composition, relative-position invariance).
 
 Parity status: every function here is pinned by tests under tests/ (see
 tests/test_oracle_*.py) except where a docstring says "parity unpinned".
@@ -337,6 +349,45 @@ def attend(Q: np.ndarray, K_mem: Sequence[np.ndarray], V_mem: Sequence[np.ndarra
             O[q0:q0 + q_block, h, :] = (P @ Vh) / denom
             LSE[h, q0:q0 + q_block] = (m + np.log(denom))[:, 0]
     return O, LSE
+
+
+# ---------------------------------------------------------------------------
+# Temporal RoPE re-indexing (Sec. 3.3 "Boundary and positional handling").
+# ---------------------------------------------------------------------------
+
+def rope_angles(index: float, pairs: int, theta: float) -> np.ndarray:
+    """Angle of pair k = 0..P-1 at temporal `index`: index * theta**(-k/P) (fp64)."""
+    k = np.arange(pairs, dtype=np.float64)
+    return float(index) * np.power(float(theta), -k / float(pairs))
+
+
+def rope_rotate(X: np.ndarray, index: float, pairs: int, theta: float, storage: Optional[str] = None) -> np.ndarray:
+    """Rotate pairs (2k, 2k+1), k < P, of the last axis of X by rope_angles:
+    (x0, x1) -> (x0 c - x1 s, x0 s + x1 c), products and sums in fp64; the
+    other dimensions are unchanged.  storage: round the result once to
+    "bf16" or "f32", or keep fp64 (None)."""
+    Y = np.array(X, dtype=np.float64, copy=True)
+    if pairs > 0:
+        a = rope_angles(index, pairs, theta)
+        c, s = np.cos(a), np.sin(a)
+        x0 = Y[..., 0:2 * pairs:2].copy()
+        x1 = Y[..., 1:2 * pairs:2].copy()
+        Y[..., 0:2 * pairs:2] = x0 * c - x1 * s
+        Y[..., 1:2 * pairs:2] = x0 * s + x1 * c
+    if storage == "bf16":
+        return round_to_bf16(Y)
+    if storage == "f32":
+        return round_to_f32(Y)
+    return Y
+
+
+def exposed_kv_rope(cache: "OracleCache", pairs: int, theta: float) -> Tuple[List[np.ndarray], List[np.ndarray]]:
+    """The memory as attention sees it with temporal RoPE handling: entry i's
+    keys rotated to temporal index i (and rounded to the storage type, as the
+    library's exposed copy is), values unchanged.  Parity unpinned as to the
+    paper's mapping (see the module docstring)."""
+    K = [rope_rotate(e.K, i, pairs, theta, cache.storage) for i, e in enumerate(cache.entries)]
+    return K, [e.V for e in cache.entries]
 
 
 def chunk_step(cache: OracleCache, Q: np.ndarray, K_chunk: np.ndarray, V_chunk: np.ndarray,

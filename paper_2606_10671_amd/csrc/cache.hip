@@ -596,6 +596,84 @@ __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Temporal RoPE view (Sec. 3.3 "Boundary and positional handling"): memory
+// keys are stored without their temporal phase; for attention, entry e is
+// exposed at temporal index e.  This kernel writes entry e's K with pairs
+// k < P rotated by the angle e * w_k, w_k = theta^(-k/P) (fp64, rounded once
+// to the storage type), and its V unchanged, into view slot e, so the
+// attention kernels read the view through an identity slot table.
+// grid = (blocks per plane, entries * 2): y = entry * 2 + kv.
+// ---------------------------------------------------------------------------
+
+struct RopeViewArgs {
+  const char* kv_layer_base;  // pool + kv_offset(layer, 0, 0)
+  const int32_t* order;       // logical -> slot
+  char* view;                 // view slot e at view + e * 2 * blk_stride (K, then V)
+  int32_t* view_order;        // identity table written here
+  size_t slot_stride;         // 2 * blk_stride
+  size_t blk_stride;
+  int64_t units;              // 16-byte units per K (or V) block
+  int n_entries;
+  int head_dim;
+  int pairs;                  // P
+  double theta;
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void rope_view_kernel(RopeViewArgs a) {
+#pragma clang fp contract(off)
+  __shared__ double cs[64], sn[64];
+  const int e = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = tid; i < a.n_entries; i += 256) a.view_order[i] = i;
+  const u32x4* src = reinterpret_cast<const u32x4*>(a.kv_layer_base + size_t(a.order[e]) * a.slot_stride +
+                                                    size_t(kv) * a.blk_stride);
+  u32x4* dst = reinterpret_cast<u32x4*>(a.view + size_t(e) * a.slot_stride + size_t(kv) * a.blk_stride);
+  const int64_t stride = int64_t(gridDim.x) * 256;
+  if (kv == 1) {  // V: unchanged
+    for (int64_t u = int64_t(blockIdx.x) * 256 + tid; u < a.units; u += stride)
+      __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
+    return;
+  }
+  if (tid < a.pairs) {
+    const double w = pow(a.theta, -double(tid) / double(a.pairs));
+    const double ang = double(e) * w;
+    cs[tid] = cos(ang);
+    sn[tid] = sin(ang);
+  }
+  __syncthreads();
+  constexpr int kElts = BF16 ? 8 : 4;  // elements per 16-byte unit (whole pairs)
+  const int units_per_head = a.head_dim / kElts;
+  for (int64_t u = int64_t(blockIdx.x) * 256 + tid; u < a.units; u += stride) {
+    u32x4 x = __builtin_nontemporal_load(src + u);
+    const int d0 = int(u % units_per_head) * kElts;  // first element of the unit within its head
+    if (d0 < 2 * a.pairs) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (BF16) {
+          const int k = (d0 >> 1) + w;  // the word holds pair k: (element 2k, element 2k+1)
+          if (k < a.pairs) {
+            const double x0 = bf16_lo(x[w]), x1 = bf16_hi(x[w]);
+            x[w] = pack_bf16_rne(x0 * cs[k] - x1 * sn[k], x0 * sn[k] + x1 * cs[k]);
+          }
+        } else {
+          if (w % 2 == 0) {
+            const int k = (d0 >> 1) + w / 2;
+            if (k < a.pairs) {
+              const double x0 = double(__uint_as_float(x[w])), x1 = double(__uint_as_float(x[w + 1]));
+              x[w] = __float_as_uint(float(x0 * cs[k] - x1 * sn[k]));
+              x[w + 1] = __float_as_uint(float(x0 * sn[k] + x1 * cs[k]));
+            }
+          }
+        }
+      }
+    }
+    __builtin_nontemporal_store(x, dst + u);
+  }
+}
+
 constexpr int kMergeUnroll = 4;
 
 // Blocks per (layer, kv) plane for a streaming pass over `units` 16-byte
@@ -653,6 +731,8 @@ bool valid_config(const fademem_config* c) {
   if (c->dtype != FADEMEM_F32 && c->dtype != FADEMEM_BF16) return false;
   if (c->merge_op < FADEMEM_MERGE_SQRT_SPAN || c->merge_op > FADEMEM_MERGE_MAX) return false;
   if (c->layers < 1 || c->layers > 4096) return false;
+  if (c->rope_pairs < 0 || c->rope_pairs > c->head_dim / 2) return false;
+  if (c->rope_pairs > 0 && !(c->rope_theta > 1.0 && c->rope_theta < 1e300)) return false;
   return true;
 }
 
@@ -682,7 +762,10 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
   L.blk_stride = round_up(L.blk_bytes, 256);
   L.off_ws = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
   L.ws_bytes = cfg->dtype == FADEMEM_BF16 ? attend_ws_bytes(cfg->head_dim) : 0;
-  L.total = L.off_ws + L.ws_bytes;
+  L.off_view = round_up(L.off_ws + L.ws_bytes, 256);
+  L.view_bytes = cfg->rope_pairs > 0 ? size_t(cfg->budget) * 2 * L.blk_stride + round_up(4 * size_t(cfg->budget), 256)
+                                     : 0;
+  L.total = L.off_view + L.view_bytes;
   *lay = L;
   return FADEMEM_OK;
 }
@@ -941,6 +1024,30 @@ int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tok
   a.head_dim = c->cfg.head_dim;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf(float(c->cfg.head_dim));
   (void)hipGetLastError();
+  if (c->cfg.rope_pairs > 0 && c->count > 0) {
+    // Expose the memory re-indexed: a rotated K (and copied V) view of the
+    // held entries, read through an identity slot table.
+    RopeViewArgs r;
+    r.kv_layer_base = a.kv_layer_base;
+    r.order = a.order;
+    r.view = c->pool + c->lay.off_view;
+    r.view_order = reinterpret_cast<int32_t*>(c->pool + c->lay.off_view + size_t(c->cfg.budget) * 2 * c->lay.blk_stride);
+    r.slot_stride = 2 * c->lay.blk_stride;
+    r.blk_stride = c->lay.blk_stride;
+    r.units = int64_t(c->lay.blk_bytes / 16);
+    r.n_entries = int(c->count);
+    r.head_dim = c->cfg.head_dim;
+    r.pairs = c->cfg.rope_pairs;
+    r.theta = c->cfg.rope_theta;
+    auto vk = c->cfg.dtype == FADEMEM_BF16 ? rope_view_kernel<true> : rope_view_kernel<false>;
+    const unsigned planes = unsigned(2 * c->count);
+    const dim3 grid(stream_blocks_per_plane(reinterpret_cast<const void*>(vk), planes, r.units, 4), planes);
+    hipLaunchKernelGGL(vk, grid, dim3(256), 0, as_stream(stream), r);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(c, e);
+    a.kv_layer_base = r.view;
+    a.order = r.view_order;
+  }
   hipError_t e = (c->cfg.dtype == FADEMEM_BF16) ? launch_attend_bf16(a, as_stream(stream))
                                                 : launch_attend_f32(a, as_stream(stream));
   if (e != hipSuccess) return hip_fail(c, e);

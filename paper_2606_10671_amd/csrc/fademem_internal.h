@@ -80,7 +80,9 @@ struct Layout {
   size_t row_elems;       // H*D: elements per token row
   size_t off_ws;          // attention scratch (bf16 caches), after the KV region
   size_t ws_bytes;        // attend_ws_bytes(D) for bf16, 0 for fp32
-  size_t total;           // off_ws + ws_bytes
+  size_t off_view;        // RoPE view: M slots of K (rotated) and V, then an identity slot table
+  size_t view_bytes;      // 0 when rope_pairs = 0
+  size_t total;           // off_view + view_bytes
 };
 
 int compute_layout(const fademem_config* cfg, Layout* lay);

@@ -48,6 +48,8 @@ class fademem_config(ctypes.Structure):
         ("merge_op", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
         ("layers", ctypes.c_int32),
+        ("rope_pairs", ctypes.c_int32),
+        ("rope_theta", ctypes.c_double),
     ]
 
 
@@ -117,9 +119,11 @@ def _ok(rc: int, where: str) -> None:
 
 def make_config(budget: int, heads: int, head_dim: int, tokens_per_block: int, beta: float = 0.3,
                 anchor: bool = True, dtype: int = FADEMEM_BF16, layers: int = 1,
-                merge_op: int = FADEMEM_MERGE_SQRT_SPAN) -> fademem_config:
+                merge_op: int = FADEMEM_MERGE_SQRT_SPAN, rope_pairs: int = 0,
+                rope_theta: float = 10000.0) -> fademem_config:
     return fademem_config(budget=budget, heads=heads, head_dim=head_dim, tokens_per_block=tokens_per_block,
-                          beta=beta, anchor=int(anchor), merge_op=merge_op, dtype=dtype, layers=layers)
+                          beta=beta, anchor=int(anchor), merge_op=merge_op, dtype=dtype, layers=layers,
+                          rope_pairs=rope_pairs, rope_theta=rope_theta)
 
 
 # -- the C calls, same names ---------------------------------------------------
@@ -230,7 +234,8 @@ class Cache:
     """
 
     def __init__(self, budget: int, heads: int, head_dim: int, tokens_per_block: int, beta: float = 0.3,
-                 anchor: bool = True, dtype=None, layers: int = 1, device=None, merge_op: str = "sqrt_span"):
+                 anchor: bool = True, dtype=None, layers: int = 1, device=None, merge_op: str = "sqrt_span",
+                 rope_pairs: int = 0, rope_theta: float = 10000.0):
         import torch
         dtype = torch.bfloat16 if dtype is None else dtype
         if dtype not in (torch.float32, torch.bfloat16):
@@ -240,7 +245,7 @@ class Cache:
         self.torch_dtype = dtype
         self.cfg = make_config(budget, heads, head_dim, tokens_per_block, beta, anchor,
                                FADEMEM_BF16 if dtype == torch.bfloat16 else FADEMEM_F32, layers,
-                               merge_op=MERGE_OPS[merge_op])
+                               merge_op=MERGE_OPS[merge_op], rope_pairs=rope_pairs, rope_theta=rope_theta)
         self.device = torch.device("cuda") if device is None else torch.device(device)
         self.pool_bytes = fademem_pool_bytes(self.cfg)
         self.pool = torch.empty(self.pool_bytes, dtype=torch.uint8, device=self.device)

@@ -61,14 +61,20 @@ def test_pool_bytes_layout():
     assert nf - n == 22 * 2 * blk - ws
     n64 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "head_dim": 64}))
     assert n - n64 == 22 * blk + ws - 2 * 512 * (128 * 64 + 2 * 256) * 4
+    # temporal RoPE handling adds the exposed copy of M entries' K and V
+    nr = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "rope_pairs": 22}))
+    assert 21 * 2 * blk <= nr - n < 21 * 2 * blk + 64 * 1024
 
 
 @pytest.mark.parametrize("field,value", [("budget", 1), ("budget", 1024), ("heads", 0), ("head_dim", 96),
                                          ("tokens_per_block", 0), ("beta", 0.0), ("beta", 1.0001),
                                          ("beta", float("nan")), ("anchor", 2), ("dtype", 7), ("layers", 0),
-                                         ("merge_op", -1), ("merge_op", 4)])
+                                         ("merge_op", -1), ("merge_op", 4), ("rope_pairs", -1),
+                                         ("rope_pairs", 65), ("rope_theta", 1.0)])
 def test_bad_configs_are_rejected(field, value):
     cfg = fm.make_config(**GOOD)
+    if field == "rope_theta":
+        cfg.rope_pairs = 22
     setattr(cfg, field, value)
     with pytest.raises(fm.FademError) as e:
         fm.fademem_pool_bytes(cfg)
