@@ -167,3 +167,75 @@ def test_explicit_scale_and_null_lse():
     out = cache.attend(dev(q), dev(kc), dev(vc), scale=0.05)
     O_ref, L_ref = attend(q, *oc.exposed_kv(), kc, vc, scale=float(np.float32(0.05)))
     check_attention(to_np(out), None, O_ref, L_ref, "bf16")
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_maximum_budget(fused):
+    """M = 1023, the largest budget (the schedule runs over 1024 entries in
+    one block): 1100 frames of 4 tokens, state and every entry bit for bit,
+    then attention over 1023 entries through the short-entry row path."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    H, D, N, M, T, F = 1, 64, 4, 1023, 1100, 4
+    print(f"max budget M={M} N={N} frames={T} fused={fused}", flush=True)
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=torch.bfloat16)
+    oc = OracleCache(budget=M, beta=0.3, anchor=True, storage="bf16")
+    gen = NumpyWanStream(31, N, H, D)
+    frames = [gen.frame() for _ in range(T)]
+    kd = torch.from_numpy(np.concatenate([f[0] for f in frames])).to("cuda", torch.bfloat16)
+    vd = torch.from_numpy(np.concatenate([f[1] for f in frames])).to("cuda", torch.bfloat16)
+    for t0 in range(0, T, F):
+        if fused:
+            cache.update(kd[t0 * N:(t0 + F) * N], vd[t0 * N:(t0 + F) * N], t0)
+        else:
+            for t in range(t0, t0 + F):
+                cache.insert(kd[t * N:(t + 1) * N], vd[t * N:(t + 1) * N], t)
+                cache.consolidate()
+        for t in range(t0, t0 + F):
+            oc.update(frames[t][0], frames[t][1], t)
+    check_state(cache, oc)
+    check_entries(cache, oc)
+    total, log = cache.merge_log()
+    assert total == T - M and log == oc.merge_log[-len(log):]
+    q = gen.queries(96)
+    kc, vc = gen.frame()
+    lse = torch.empty((H, 96), dtype=torch.float32, device="cuda")
+    out = cache.attend(dev(q), dev(kc), dev(vc), lse=lse)
+    O_ref, L_ref = attend(q, *oc.exposed_kv(), kc, vc)
+    check_attention(to_np(out), to_np(lse), O_ref, L_ref, "bf16")
+
+
+def test_more_layers_than_one_launch():
+    """70 layers: inserts, merges and fused updates go out in launches of at
+    most 64 layers; layers 0, 63, 64 and 69 are checked against the oracle."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    H, D, N, M, F, L = 1, 64, 16, 3, 2, 70
+    print(f"layers={L} M={M} N={N}", flush=True)
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.5, anchor=False, dtype=torch.bfloat16,
+                  layers=L)
+    track = (0, 63, 64, 69)
+    ocs = {l: OracleCache(budget=M, beta=0.5, anchor=False, storage="bf16") for l in track}
+    gens = [NumpyWanStream(40 + l, N, H, D) for l in range(L)]
+    for c in range(7):
+        frames = [[g.frame() for _ in range(F)] for g in gens]
+        kch = [dev(np.concatenate([f[0] for f in fr])) for fr in frames]
+        vch = [dev(np.concatenate([f[1] for f in fr])) for fr in frames]
+        if c % 2:
+            cache.update(kch, vch, c * F)
+        else:
+            for f in range(F):
+                cache.insert([k[f * N:(f + 1) * N] for k in kch], [v[f * N:(f + 1) * N] for v in vch], c * F + f)
+                cache.consolidate()
+        for l in track:
+            for f in range(F):
+                ocs[l].update(frames[l][f][0], frames[l][f][1], c * F + f)
+        check_state(cache, ocs[0], where=c)
+    for l in track:
+        check_entries(cache, ocs[l], layer=l, where=l)
+        q = gens[l].queries(40)
+        out = cache.attend(dev(q), kch[l], vch[l], layer=l)
+        K = np.concatenate([f[0] for f in frames[l]])
+        V = np.concatenate([f[1] for f in frames[l]])
+        O_ref, L_ref = attend(q, *ocs[l].exposed_kv(), K, V)
+        check_attention(to_np(out), None, O_ref, L_ref, "bf16", where=l)
