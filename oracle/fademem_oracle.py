@@ -407,3 +407,90 @@ def chunk_step(cache: OracleCache, Q: np.ndarray, K_chunk: np.ndarray, V_chunk: 
         merges.append(cache.update(K_chunk[f * N:(f + 1) * N], V_chunk[f * N:(f + 1) * N],
                                    first_position + f))
     return O, LSE, merges
+
+
+# ---------------------------------------------------------------------------
+# Distance-dependent spectral decay (Sec. 3.2; supplementary Sec. S2): an
+# orthonormal 2-D DCT-II of each channel-averaged latent frame, coefficients
+# grouped by normalized radial frequency r(u, v) = sqrt((u/H)^2 + (v/W)^2),
+# the Pearson correlation C_k(lag) between band k's coefficients of frame 0
+# and of frame lag, averaged over clips; per band a decorrelation horizon,
+# and the fit r*(t) = a t^(-b) by nonlinear least squares.
+# Readings where the paper is silent: `bands` equal-width bands of r over
+# [0, max r] with the DC coefficient left out; the curve is smoothed with a
+# centred moving average of 5 lags (shrinking at the ends); the horizon is
+# the first lag, after at least half of the curve's total decay, at which
+# the smoothed curve falls by less than 5 % of its steepest one-lag fall
+# (for a decay exp(-lag/tau) that is tau*ln 20, proportional to tau); a
+# band's radius is the centre of its bin.
+# ---------------------------------------------------------------------------
+
+def dct2_ortho(Z) -> np.ndarray:
+    """Orthonormal 2-D DCT-II over the last two axes, in fp64 (library DCT)."""
+    from scipy.fft import dctn
+    return dctn(np.asarray(Z, dtype=np.float64), type=2, norm="ortho", axes=(-2, -1))
+
+
+def radial_band_of(H: int, W: int, bands: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Band index of every coefficient (u, v) as an int32 [H][W] array (-1 for
+    the DC coefficient) and the bands' centre radii."""
+    r = np.sqrt((np.arange(H)[:, None] / H) ** 2 + (np.arange(W)[None, :] / W) ** 2)
+    r_max = r.max()
+    k = np.minimum(np.floor(r / r_max * bands).astype(np.int64), bands - 1)
+    k[0, 0] = -1
+    centres = (np.arange(bands) + 0.5) * r_max / bands
+    return k.astype(np.int32), centres
+
+
+def pearson(x: np.ndarray, y: np.ndarray) -> float:
+    """Pearson correlation coefficient, by its definition, in fp64."""
+    x = np.asarray(x, np.float64)
+    y = np.asarray(y, np.float64)
+    xm = x - x.mean()
+    ym = y - y.mean()
+    return float((xm @ ym) / math.sqrt((xm @ xm) * (ym @ ym)))
+
+
+def band_correlations(latents, band_of: np.ndarray, bands: int, max_lag: int) -> np.ndarray:
+    """C_k(lag) for k < bands, lag = 0..max_lag: per clip the Pearson
+    correlation of band k's DCT coefficients of frame 0 and frame lag,
+    averaged over clips.  latents: [clips][frames][H][W]."""
+    L = np.asarray(latents)
+    out = np.zeros((bands, max_lag + 1))
+    for c in range(L.shape[0]):
+        D = dct2_ortho(L[c, :max_lag + 1])
+        for k in range(bands):
+            sel = band_of == k
+            x = D[0][sel]
+            for lag in range(max_lag + 1):
+                out[k, lag] += pearson(x, D[lag][sel])
+    return out / L.shape[0]
+
+
+def decorrelation_horizons(corr: np.ndarray, width: int = 5, drop: float = 0.05) -> np.ndarray:
+    """Per band, the lag at which the smoothed curve enters its near-flat
+    regime (the reading in the section comment); -1 if it never does."""
+    bands, n = corr.shape
+    out = np.full(bands, -1, dtype=np.int64)
+    h = width // 2
+    for k in range(bands):
+        s = np.array([corr[k, max(0, i - h):min(n, i + h + 1)].mean() for i in range(n)])
+        total = s[0] - s.min()
+        steepest = (s[:-1] - s[1:]).max() if n > 1 else 0.0
+        if not (total > 0 and steepest > 0):
+            continue
+        for lag in range(1, n - 1):
+            if s[0] - s[lag] >= 0.5 * total and s[lag] - s[lag + 1] < drop * steepest:
+                out[k] = lag
+                break
+    return out
+
+
+def fit_power_law(t: np.ndarray, r: np.ndarray) -> Tuple[float, float]:
+    """(a, b) of r = a * t^(-b) by nonlinear least squares (library solver)."""
+    from scipy.optimize import curve_fit
+    t = np.asarray(t, np.float64)
+    r = np.asarray(r, np.float64)
+    b0, la0 = np.polyfit(np.log(t), np.log(r), 1)
+    (a, b), _ = curve_fit(lambda x, a, b: a * np.power(x, -b), t, r, p0=(math.exp(la0), -b0), maxfev=10000)
+    return float(a), float(b)

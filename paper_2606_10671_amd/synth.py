@@ -110,3 +110,52 @@ class TorchWanStream:
         ks, vs = zip(*[self.frame() for _ in range(frames)])
         q = self._randn((frames * self.shape[0],) + self.shape[1:]).to(self.torch.bfloat16)
         return q, self.torch.cat(ks, 0).contiguous(), self.torch.cat(vs, 0).contiguous()
+
+
+class SpectralClips:
+    """Synthetic channel-averaged latent clips for the spectral analysis
+    (the paper's Pexels clips and Wan VAE are not available).
+
+    Each frame is a sum of smoothed random fields at several spatial scales:
+    level s is white noise box-filtered with half-width w_s (wider = lower
+    spatial frequencies), evolving over frames as an AR(1) process with
+    coefficient rho_s (wider = slower), so coarse structure stays
+    correlated over longer lags than fine structure.  ``clip()`` returns a
+    float32 tensor [frames][H][W]."""
+
+    def __init__(self, seed: int, frames: int, height: int, width: int, device="cpu",
+                 widths=(0, 1, 3, 7, 15), rhos=(0.5, 0.8, 0.93, 0.98, 0.995)):
+        import torch
+        self.torch = torch
+        self.gen = torch.Generator(device=device)
+        self.gen.manual_seed(seed)
+        self.shape = (frames, height, width)
+        self.device = device
+        self.widths, self.rhos = widths, rhos
+
+    def _box(self, x, w):
+        """Separable box filter of half-width w (replicate edges), on [T][H][W]."""
+        if w == 0:
+            return x
+        torch = self.torch
+        k = torch.ones(1, 1, 2 * w + 1, dtype=x.dtype, device=x.device) / (2 * w + 1)
+        T, H, W = x.shape
+        y = torch.nn.functional.pad(x.reshape(T * H, 1, W), (w, w), mode="replicate")
+        y = torch.nn.functional.conv1d(y, k).reshape(T, H, W).transpose(1, 2)
+        y = torch.nn.functional.pad(y.reshape(T * W, 1, H), (w, w), mode="replicate")
+        return torch.nn.functional.conv1d(y, k).reshape(T, W, H).transpose(1, 2).contiguous()
+
+    def clip(self):
+        torch = self.torch
+        T, H, W = self.shape
+        z = torch.zeros(self.shape, dtype=torch.float32, device=self.device)
+        for w, rho in zip(self.widths, self.rhos):
+            e = torch.randn(self.shape, generator=self.gen, device=self.device, dtype=torch.float32)
+            a = torch.empty_like(e)
+            a[0] = e[0]
+            b = float(np.sqrt(1.0 - rho * rho))
+            for t in range(1, T):
+                a[t] = rho * a[t - 1] + b * e[t]
+            f = self._box(a, w)
+            z += f / f.std()
+        return z
