@@ -209,6 +209,28 @@ int fademem_merge_log(fademem_cache* cache, int32_t* j, int64_t cap, int64_t* to
  * Errors: EINVAL (NULL cache), EHIP. */
 int fademem_merge_counts(fademem_cache* cache, int64_t* total, int64_t* anchor, void* stream);
 
+/* Distance-dependent spectral decay (Sec. 3.2; supplementary Sec. S2).
+ * latents: device [clips][frames][height][width] fp32, channel-averaged
+ * latent frames.  For every clip the orthonormal 2-D DCT-II of frames
+ * 0..max_lag; for every radial band k < bands and lag the Pearson
+ * correlation of band k's DCT coefficients of frame 0 and of frame lag;
+ * corr (device, [bands][max_lag+1] fp64) receives the mean over clips.
+ * band_of: device [height][width] int32, the band of DCT coefficient
+ * (u, v) (any value outside [0, bands) leaves the coefficient out).
+ * workspace: device, 256-byte aligned, at least
+ * fademem_spectral_workspace_bytes (it holds the DCT of the analysed
+ * frames).  Limits: height*width <= 40960 and the frame, its transform and
+ * both DCT bases within 160 KiB of LDS (e.g. 60 x 104); max_lag < frames,
+ * max_lag < 65535; 1 <= bands <= 1024.  Asynchronous on `stream`.  A band
+ * whose coefficients do not vary gets NaN.
+ * Errors: EINVAL (NULL/misaligned pointers, sizes out of range), ENOMEM
+ * (workspace too small), EHIP. */
+int fademem_spectral_workspace_bytes(int64_t clips, int64_t frames, int32_t height, int32_t width,
+                                     int32_t bands, int64_t max_lag, size_t* bytes);
+int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, int32_t height,
+                          int32_t width, const int32_t* band_of, int32_t bands, int64_t max_lag,
+                          void* workspace, size_t workspace_bytes, double* corr, void* stream);
+
 /* hipError_t value of the last FADEMEM_EHIP on this cache (0 if none). */
 int fademem_last_hip_error(const fademem_cache* cache);
 

@@ -33,7 +33,7 @@ EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
     "fademem_consolidate", "fademem_update", "fademem_attend", "fademem_count", "fademem_get_state",
     "fademem_entry_kv", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
-    "fademem_strerror",
+    "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr",
 )
 
 
@@ -103,6 +103,10 @@ def lib() -> ctypes.CDLL:
     L.fademem_entry_kv.argtypes = [c_void_p, c_int32, c_int64, P(c_void_p), P(c_void_p), c_void_p]
     L.fademem_merge_log.argtypes = [c_void_p, P(c_int32), c_int64, P(c_int64), c_void_p]
     L.fademem_merge_counts.argtypes = [c_void_p, P(c_int64), P(c_int64), c_void_p]
+    L.fademem_spectral_workspace_bytes.argtypes = [c_int64, c_int64, c_int32, c_int32, c_int32, c_int64,
+                                                   P(ctypes.c_size_t)]
+    L.fademem_spectral_corr.argtypes = [c_void_p, c_int64, c_int64, c_int32, c_int32, c_void_p, c_int32, c_int64,
+                                        c_void_p, ctypes.c_size_t, c_void_p, c_void_p]
     L.fademem_last_hip_error.argtypes = [c_void_p]
     for name in EXPORTED:
         if name != "fademem_strerror":
@@ -213,6 +217,23 @@ def fademem_merge_counts(handle: int, stream: int = 0):
     _ok(lib().fademem_merge_counts(ctypes.c_void_p(handle), ctypes.byref(total), ctypes.byref(anchor),
                                    ctypes.c_void_p(stream)), "fademem_merge_counts")
     return total.value, anchor.value
+
+
+def fademem_spectral_workspace_bytes(clips: int, frames: int, height: int, width: int, bands: int,
+                                     max_lag: int) -> int:
+    n = ctypes.c_size_t(0)
+    _ok(lib().fademem_spectral_workspace_bytes(clips, frames, height, width, bands, max_lag, ctypes.byref(n)),
+        "fademem_spectral_workspace_bytes")
+    return n.value
+
+
+def fademem_spectral_corr(latents_ptr: int, clips: int, frames: int, height: int, width: int, band_of_ptr: int,
+                          bands: int, max_lag: int, workspace_ptr: int, workspace_bytes: int, corr_ptr: int,
+                          stream: int = 0) -> None:
+    _ok(lib().fademem_spectral_corr(ctypes.c_void_p(latents_ptr), clips, frames, height, width,
+                                    ctypes.c_void_p(band_of_ptr), bands, max_lag, ctypes.c_void_p(workspace_ptr),
+                                    workspace_bytes, ctypes.c_void_p(corr_ptr), ctypes.c_void_p(stream)),
+        "fademem_spectral_corr")
 
 
 def fademem_last_hip_error(handle: int) -> int:
