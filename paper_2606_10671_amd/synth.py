@@ -15,6 +15,10 @@ Recipes
   with z, e i.i.d. N(0, 1); V likewise from independent draws; Q i.i.d.
   N(0, 1); all rounded to bf16.  A chunk's F frames are consecutive frames
   of the stream, so merged neighbours are correlated but not identical.
+* spectral clips (``SpectralClips``): per frame, the sum of five random
+  fields, field s being white noise box-filtered with half-width w_s and
+  evolving over frames as AR(1) with coefficient rho_s, each scaled to unit
+  standard deviation (coarse scales decorrelate slowly, fine ones fast).
 """
 from __future__ import annotations
 
