@@ -9,18 +9,28 @@
 // Kernels:
 // * dct_basis_kernel -- A_N[k][n] = s_k cos(pi (2n+1) k / (2N)), s_0 =
 //   sqrt(1/N), s_k = sqrt(2/N), in fp64, stored fp32;
+// * band_order_kernel -- the coefficients grouped by band (a stable
+//   counting sort in one block), so each band is a contiguous index list;
+// * spectral_fused_kernel (frames up to 64 x 128) -- persistent blocks, each
+//   taking an equal contiguous range of the (clip, lag) frames: per frame
+//   T = z A_W^T and D = A_H T on the fp32 matrix cores
+//   (v_mfma_f32_16x16x4_f32; wave j owns the 16 columns v of tile j), the
+//   second product taking T straight from the first one's accumulators,
+//   then D written to LDS in band order and reduced per band (fp64 sums)
+//   against frame 0's coefficients (kept in LDS) to the Pearson
+//   coefficient; no transform ever reaches HBM;
+// * clip_mean_kernel -- the mean over clips, in a fixed order (every call
+//   gives the same bits).
+// Larger frames take the general path:
 // * dct2_kernel -- one block per (clip, run of frames): both bases (as
 //   transposes) in LDS once, then per frame z^T in LDS, T = z A_W^T and
 //   D = A_H T, each thread computing 4 x 4 output tiles from 16-byte LDS
 //   reads (8 FMAs per read); fp32 products and sums; sizes padded to
 //   multiples of 4 with zeros;
-// * band_order_kernel -- the coefficients grouped by band (stable counting
-//   sort, one thread), so each band is a contiguous index list;
 // * band_corr_kernel -- one block per (clip, lag): each wave takes bands in
 //   turn, sums x, y, x^2, y^2, xy over the band in fp64 (lanes, then a wave
 //   reduction), and writes the Pearson coefficient
-//   (n Sxy - Sx Sy) / sqrt((n Sxx - Sx^2)(n Syy - Sy^2));
-// * clip_mean_kernel -- the mean over clips, in clip order (deterministic).
+//   (n Sxy - Sx Sy) / sqrt((n Sxx - Sx^2)(n Syy - Sy^2)).
 #include <math.h>
 #include <string.h>
 
@@ -38,14 +48,14 @@ struct SpecLayout {
   size_t off_ah, off_aw, off_d, off_perm, off_start, off_clip, total;
 };
 
-bool spec_layout(int64_t clips, int64_t nlag, int64_t H, int64_t W, int64_t bands, SpecLayout* L) {
-  const double d_bytes = double(clips) * double(nlag) * double(H) * double(W) * 4.0;
+bool spec_layout(int64_t clips, int64_t nlag, int64_t H, int64_t W, int64_t bands, bool fused, SpecLayout* L) {
+  const double d_bytes = fused ? 0.0 : double(clips) * double(nlag) * double(H) * double(W) * 4.0;
   const double c_bytes = double(clips) * double(nlag) * double(bands) * 8.0;
   if (d_bytes > 1e15 || c_bytes > 1e15) return false;
   size_t off = 0;
   L->off_ah = off;    off = rup(off + size_t(H * H) * 4);
   L->off_aw = off;    off = rup(off + size_t(W * W) * 4);
-  L->off_d = off;     off = rup(off + size_t(clips) * size_t(nlag) * size_t(H * W) * 4);
+  L->off_d = off;     off = rup(off + (fused ? 0 : size_t(clips) * size_t(nlag) * size_t(H * W) * 4));
   L->off_perm = off;  off = rup(off + size_t(H * W) * 4);
   L->off_start = off; off = rup(off + size_t(bands + 1) * 4);
   L->off_clip = off;  off = rup(off + size_t(clips) * size_t(nlag) * size_t(bands) * 8);
@@ -143,54 +153,61 @@ __global__ __launch_bounds__(kDctThreads) void dct2_kernel(const float* latents,
   }
 }
 
+// Exclusive prefix sum over the block (all threads must call it); *total
+// gets the sum of every thread's value.
+__device__ int block_exclusive_scan(int v, int32_t* wsum, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();  // wsum is free
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int w = 0; w < nw; ++w) {
+    const int t = wsum[w];
+    if (w < wave) before += t;
+    all += t;
+  }
+  *total = all;
+  return before + x - v;
+}
+
 // Coefficient indices grouped by band, in index order within a band;
 // entries outside [0, bands) are left out.  One block of 1024 threads with
-// the band map in LDS: thread t takes band t / C in chunk t % C of the map
-// (C = chunks per band), counts it, then after a prefix over (band, chunk)
-// writes that chunk's indices of that band in order.
+// the band map in LDS: thread t counts band t / C in chunk t % C of the map
+// (C = 1024 / bands chunks per band), a block prefix sum gives each (band,
+// chunk) its first position, and the thread writes that chunk's indices of
+// the band in order.
 constexpr int kOrderMaxHW = 40960;
 constexpr int kOrderThreads = 1024;
 __global__ __launch_bounds__(kOrderThreads) void band_order_kernel(const int32_t* band_of, int HW, int bands,
                                                                    int32_t* perm, int32_t* start) {
   __shared__ int16_t map[kOrderMaxHW];
-  __shared__ int32_t cnt[kOrderThreads];
+  __shared__ int32_t wsum[kOrderThreads / 64];
   const int tid = threadIdx.x;
   for (int i = tid; i < HW; i += kOrderThreads) {
     const int b = band_of[i];
     map[i] = int16_t((b >= 0 && b < bands) ? b : -1);
   }
-  const int C = bands >= kOrderThreads ? 1 : kOrderThreads / bands;  // chunks per band
-  const int per_round = kOrderThreads / C;                           // bands per round
+  const int C = kOrderThreads / bands;  // bands <= 1024
+  const int b = tid / C, j = tid % C;
+  const bool on = b < bands;
   const int len = (HW + C - 1) / C;
-  for (int b0 = 0; b0 < bands; b0 += per_round) {
-    const int b = b0 + tid / C, j = tid % C;
-    const bool on = tid / C < per_round && b < bands;
-    const int i0 = j * len, i1 = min(HW, i0 + len);
-    __syncthreads();
-    int n = 0;
-    if (on)
-      for (int i = i0; i < i1; ++i) n += (map[i] == b);
-    cnt[tid] = n;
-    __syncthreads();
-    if (tid == 0) {
-      int acc = b0 == 0 ? 0 : start[b0];
-      for (int t = 0; t < per_round * C; ++t) {
-        const int bt = b0 + t / C;
-        if (bt >= bands) break;
-        if (t % C == 0) start[bt] = acc;
-        const int m = cnt[t];
-        cnt[t] = acc;
-        acc += m;
-      }
-      start[min(bands, b0 + per_round)] = acc;
-    }
-    __syncthreads();
-    if (on) {
-      int pos = cnt[tid];
-      for (int i = i0; i < i1; ++i)
-        if (map[i] == b) perm[pos++] = i;
-    }
-  }
+  const int i0 = min(HW, j * len), i1 = min(HW, i0 + len);
+  __syncthreads();
+  int n = 0;
+  if (on)
+    for (int i = i0; i < i1; ++i) n += (map[i] == b);
+  int total;
+  int pos = block_exclusive_scan(n, wsum, &total);
+  if (on && j == 0) start[b] = pos;
+  if (tid == 0) start[bands] = total;
+  if (on)
+    for (int i = i0; i < i1; ++i)
+      if (map[i] == b) perm[pos++] = i;
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -232,13 +249,336 @@ __global__ __launch_bounds__(256) void band_corr_kernel(const float* D, int nlag
   }
 }
 
-__global__ void clip_mean_kernel(const double* per_clip, int64_t clips, int nlag, int bands, double* corr) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;  // i = band * nlag + lag
-  if (i >= int64_t(bands) * nlag) return;
-  const int b = int(i / nlag), lag = int(i % nlag);
+// ---- fused path: frames of up to 64 x 128 ------------------------------
+constexpr int kFusedThreads = 512;  // 8 waves; wave j owns v-tile j (16 columns)
+constexpr int kFusedMaxH = 64, kFusedMaxW = 128;
+
+__host__ __device__ inline int fused_zl_stride(int W) { return (W + 15) / 16 * 16 + 4; }
+__host__ __device__ inline int r16(int x) { return (x + 15) / 16 * 16; }
+
+// Byte offsets of the fused kernel's LDS regions.  zl: the frame, [16 HT]
+// rows of stride S = 16 n + 4 floats (zero outside H x W), so that the
+// 16-byte reads of 16 consecutive rows fall in distinct banks; dl: the
+// transform D in band order (at set-up, the inverse of the band order);
+// xl: frame 0's coefficients in band order; ahl: A_H as the second
+// product's A fragments; sl: the band starts; sxl: per band, frame 0's sum
+// and sum of squares.
+struct FusedLds {
+  int zl, dl, xl, ahl, sl, sxl, total;
+};
+__host__ __device__ inline FusedLds fused_lds(int H, int W, int bands) {
+  const int HT = (H + 15) / 16;
+  FusedLds L;
+  int off = 0;
+  L.zl = off;  off += r16(16 * HT * fused_zl_stride(W) * 4);
+  L.dl = off;  off += r16(H * W * 4 + 4);  // + a spare slot that takes left-out coefficients
+  L.xl = off;  off += r16(H * W * 4);
+  L.ahl = off; off += r16(HT * HT * 256 * 4);
+  L.sl = off;  off += r16((bands + 1) * 4);
+  L.sxl = off; off += r16(bands * 16);
+  L.total = off;
+  return L;
+}
+
+bool fused_fits(int64_t H, int64_t W, int64_t bands) {
+  return H <= kFusedMaxH && W <= kFusedMaxW && fused_lds(int(H), int(W), int(bands)).total <= kSpecLdsBytes;
+}
+
+// fp64 lane -> lane moves within rows of 16 (DPP), on the two halves.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, int(b), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, int(b >> 32), CTRL, 0xf, 0xf, false);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane(int(b), l), hi = __builtin_amdgcn_readlane(int(b >> 32), l);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+}
+// Sum over the 64 lanes in a fixed order (every lane gets the same bits):
+// pairs, quads, eights and sixteens within each row, then the four rows.
+__device__ __forceinline__ double wave_total(double v) {
+  v += dpp_f64<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_f64<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_f64<0x141>(v);  // row_half_mirror
+  v += dpp_f64<0x140>(v);  // row_mirror
+  return (lane_f64(v, 0) + lane_f64(v, 16)) + (lane_f64(v, 32) + lane_f64(v, 48));
+}
+
+// v_mfma_f32_16x16x4_f32 lane layout (64 lanes, l = lane): A operand
+// A[l % 16][l / 16], B operand B[l / 16][l % 16], result element r of lane l
+// is C[4 (l / 16) + r][l % 16].  The contraction index k of one step can be
+// any 4 values of the summed index, as long as A and B agree:
+// * T = z A_W^T, step (q, e): k = w = 16 q + 4 (l / 16) + e, so lane l reads
+//   z[h][16 q + 4 (l / 16) .. + 3] with one 16-byte LDS read for 4 steps, and
+//   holds B = A_W[v][w] for its own v-tile in registers for the whole run;
+// * D = A_H T, step (i, r): k = h = 16 i + 4 (l / 16) + r, which is where
+//   element r of lane l of T's tile i already sits: T feeds the second
+//   product from its accumulators with no data movement.
+// Each lane writes its D values straight to their band-order positions, so
+// a band is a contiguous run of dl and xl.  Band b is always reduced by wave
+// b % 8, which also keeps frame 0's run and sums for it: those need no
+// barrier.
+template <int HT, int NQ>
+__global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const float* latents, int64_t frames, int nlag,
+                                                                       int64_t clips, int H, int W, const float* AH,
+                                                                       const float* AW, const int32_t* perm,
+                                                                       const int32_t* start, int bands,
+                                                                       double* per_clip) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const FusedLds L = fused_lds(H, W, bands);
+  float* zl = reinterpret_cast<float*>(smem + L.zl);
+  float* dl = reinterpret_cast<float*>(smem + L.dl);
+  int32_t* inv = reinterpret_cast<int32_t*>(smem + L.dl);  // set-up only
+  float* xl = reinterpret_cast<float*>(smem + L.xl);
+  float* ahl = reinterpret_cast<float*>(smem + L.ahl);
+  int32_t* sl = reinterpret_cast<int32_t*>(smem + L.sl);
+  double* sxl = reinterpret_cast<double*>(smem + L.sxl);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int S = fused_zl_stride(W);  // NQ = (W + 15) / 16 quads of 16 columns = v-tiles
+  const int HW = H * W;
+  const int nperm = start[bands];
+  const bool mma = wave < NQ;
+  const int vcol = 16 * wave + (lane & 15);
+
+  for (int i = tid; i < 16 * HT * S; i += kFusedThreads) zl[i] = 0.0f;
+  for (int i = tid; i < HT * HT * 256; i += kFusedThreads) {  // [a][i][lane][r]
+    const int r = i & 3, l = (i >> 2) & 63, ai = i >> 8;
+    const int a = ai / HT, it = ai % HT;
+    const int u = 16 * a + (l & 15), h = 16 * it + 4 * (l >> 4) + r;
+    ahl[i] = (u < H && h < H) ? AH[u * H + h] : 0.0f;
+  }
+  for (int i = tid; i <= bands; i += kFusedThreads) sl[i] = start[i];
+  for (int i = tid; i < HW; i += kFusedThreads) inv[i] = -1;
+  f32x4 bw[NQ];  // bw[q][e] = A_W[v][16 q + 4 (l / 16) + e]
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int w = 16 * q + 4 * (lane >> 4) + e;
+      bw[q][e] = (mma && vcol < W && w < W) ? AW[vcol * W + w] : 0.0f;
+    }
+  __syncthreads();
+  for (int j = tid; j < nperm; j += kFusedThreads) inv[perm[j]] = j;
+  __syncthreads();
+  int pos[4 * HT];  // band-order position of result element (a, r) of this lane; HW (spare) if left out
+#pragma unroll
+  for (int a = 0; a < HT; ++a)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int u = 16 * a + 4 * (lane >> 4) + r;
+      const int p = (mma && u < H && vcol < W) ? inv[u * W + vcol] : -1;
+      pos[4 * a + r] = p >= 0 ? p : HW;
+    }
+  // This block's frames: an equal contiguous share of the (clip, lag) order,
+  // preceded by frame 0 of its first clip when the share starts past it.
+  const int64_t total = clips * int64_t(nlag);
+  const int64_t f0 = total * blockIdx.x / gridDim.x, f1 = total * (blockIdx.x + 1) / gridDim.x;
+  const int64_t c_first = f0 / nlag;
+  const int t_first = int(f0 - c_first * nlag);
+  const int64_t njobs = (f1 - f0) + (t_first != 0 ? 1 : 0);
+  // Frame loads: W % 4 == 0 as float4 chunks of the contiguous frame (chunk
+  // tid + 512 k), else one float per (row, column) with column tid % 128.
+  const bool vec = (W & 3) == 0;
+  constexpr int kChunks = HT;  // float4 chunks per thread: H W <= 16 HT x 128 = 2048 HT floats
+  static_assert(kChunks * kFusedThreads * 4 >= 16 * HT * kFusedMaxW, "chunk count");
+  int zoff[kChunks];  // LDS offset of each chunk, or -1
+#pragma unroll
+  for (int k = 0; k < kChunks; ++k) {
+    const int e = 4 * (tid + kFusedThreads * k);
+    zoff[k] = (vec && e < HW) ? (e / W) * S + e % W : -1;
+  }
+  const int cz = tid & 127, rz = tid >> 7;
+  f32x4 zr[HT];  // vec: chunk k in zr[k]; else row rz + 4 k in zr[k / 4][k % 4]
+  auto load_z = [&](int64_t c, int t) {
+    const float* z = latents + (size_t(c) * size_t(frames) + size_t(t)) * size_t(HW);
+    if (vec) {
+#pragma unroll
+      for (int k = 0; k < kChunks; ++k)
+        if (zoff[k] >= 0) zr[k] = *reinterpret_cast<const f32x4*>(z + 4 * (tid + kFusedThreads * k));
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4 * HT; ++k) {
+        const int h = rz + 4 * k;
+        zr[k / 4][k % 4] = (cz < W && h < H) ? z[h * W + cz] : 0.0f;
+      }
+    }
+  };
+  auto store_z = [&]() {
+    if (vec) {
+#pragma unroll
+      for (int k = 0; k < kChunks; ++k)
+        if (zoff[k] >= 0) *reinterpret_cast<f32x4*>(zl + zoff[k]) = zr[k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4 * HT; ++k) {
+        const int h = rz + 4 * k;
+        if (cz < W && h < H) zl[h * S + cz] = zr[k / 4][k % 4];
+      }
+    }
+  };
+  // current job (c, t); the first is frame 0 of c_first (no output) when the
+  // share starts past it
+  int64_t c = c_first;
+  int t = 0;
+  bool emit = t_first == 0;
+  load_z(c, t);
+  __syncthreads();  // every lane has read its positions from inv
+  store_z();
+  __syncthreads();
+  auto zfrag = [&](f32x4* a, int q) {
+#pragma unroll
+    for (int i = 0; i < HT; ++i)
+      a[i] = *reinterpret_cast<const f32x4*>(zl + (16 * i + (lane & 15)) * S + 16 * q + 4 * (lane >> 4));
+  };
+  for (int64_t k = 0; k < njobs; ++k) {
+    const bool more = k + 1 < njobs;
+    int64_t cn = c;
+    int tn = t + 1;
+    if (!emit) {
+      tn = t_first;
+    } else if (tn == nlag) {
+      cn = c + 1;
+      tn = 0;
+    }
+    if (more) load_z(cn, tn);
+    f32x4 dacc[HT];
+    if (mma) {
+      f32x4 tacc[HT], acur[HT];
+#pragma unroll
+      for (int i = 0; i < HT; ++i) tacc[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        zfrag(acur, q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < HT; ++i)
+            tacc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(acur[i][e], bw[q][e], tacc[i], 0, 0, 0);
+      }
+#pragma unroll
+      for (int a = 0; a < HT; ++a) dacc[a] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int i = 0; i < HT; ++i) {
+        f32x4 ah[HT];
+#pragma unroll
+        for (int a = 0; a < HT; ++a) ah[a] = *reinterpret_cast<const f32x4*>(ahl + ((a * HT + i) * 64 + lane) * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int a = 0; a < HT; ++a)
+            dacc[a] = __builtin_amdgcn_mfma_f32_16x16x4f32(ah[a][r], tacc[i][r], dacc[a], 0, 0, 0);
+      }
+    }
+    __syncthreads();  // every read of zl, and the previous frame's band sums, are done
+    if (mma) {
+#pragma unroll
+      for (int a = 0; a < HT; ++a)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          dl[pos[4 * a + r]] = dacc[a][r];
+    }
+    if (more) store_z();
+    __syncthreads();
+    double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(t)) * size_t(bands);
+    for (int b = wave; b < bands; b += kFusedThreads / 64) {
+      const int s0 = sl[b], s1 = sl[b + 1];
+      double sx, sxx, sy = 0, syy = 0, sxy = 0;
+      if (t == 0) {  // frame 0 of a clip: its run becomes x
+        for (int j = s0 + lane; j < s1; j += 64) {
+          const float yf = dl[j];
+          xl[j] = yf;
+          const double y = yf;
+          sy += y;
+          syy = fma(y, y, syy);
+        }
+        sy = wave_total(sy);
+        syy = wave_total(syy);
+        sx = sy;
+        sxx = syy;
+        sxy = syy;
+        if (lane == 0) {
+          sxl[2 * b] = sx;
+          sxl[2 * b + 1] = sxx;
+        }
+      } else {
+        int j = s0 + lane;
+        for (; j + 192 < s1; j += 256) {  // four elements per lane in flight
+          float xf[4], yf[4];
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            xf[m] = xl[j + 64 * m];
+            yf[m] = dl[j + 64 * m];
+          }
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const double x = xf[m], y = yf[m];
+            sy += y;
+            syy = fma(y, y, syy);
+            sxy = fma(x, y, sxy);
+          }
+        }
+        for (; j < s1; j += 64) {
+          const double x = xl[j], y = dl[j];
+          sy += y;
+          syy = fma(y, y, syy);
+          sxy = fma(x, y, sxy);
+        }
+        sy = wave_total(sy);
+        syy = wave_total(syy);
+        sxy = wave_total(sxy);
+        sx = sxl[2 * b];
+        sxx = sxl[2 * b + 1];
+      }
+      if (emit && lane == 0) {
+        const double n = double(s1 - s0);
+        const double cov = n * sxy - sx * sy;
+        const double vx = n * sxx - sx * sx, vy = n * syy - sy * sy;
+        out[b] = cov / sqrt(vx * vy);  // NaN for a band without spread
+      }
+    }
+    c = cn;
+    t = tn;
+    emit = true;
+  }
+}
+
+typedef void (*FusedKernel)(const float*, int64_t, int, int64_t, int, int, const float*, const float*,
+                            const int32_t*, const int32_t*, int, double*);
+template <int HT>
+constexpr FusedKernel kFusedRow[8] = {spectral_fused_kernel<HT, 1>, spectral_fused_kernel<HT, 2>,
+                                      spectral_fused_kernel<HT, 3>, spectral_fused_kernel<HT, 4>,
+                                      spectral_fused_kernel<HT, 5>, spectral_fused_kernel<HT, 6>,
+                                      spectral_fused_kernel<HT, 7>, spectral_fused_kernel<HT, 8>};
+FusedKernel fused_kernel(int H, int W) {  // H <= 64, W <= 128
+  const int HT = (H + 15) / 16, q = (W + 15) / 16 - 1;
+  return HT == 1 ? kFusedRow<1>[q] : HT == 2 ? kFusedRow<2>[q] : HT == 3 ? kFusedRow<3>[q] : kFusedRow<4>[q];
+}
+
+// Mean over clips of per_clip[clip][lag][band] into corr[band][lag].  Block
+// = 16 consecutive (lag, band) outputs x 16 clip groups: group g sums clips
+// g, g + 16, ... in order, then the 16 partial sums are added in group order
+// (a fixed order, so every call gives the same bits).
+constexpr int kMeanOuts = 16, kMeanGroups = 16;
+__global__ __launch_bounds__(kMeanOuts * kMeanGroups) void clip_mean_kernel(const double* per_clip, int64_t clips,
+                                                                           int nlag, int bands, double* corr) {
+  __shared__ double part[kMeanGroups][kMeanOuts];
+  const int o = threadIdx.x % kMeanOuts, g = threadIdx.x / kMeanOuts;
+  const int64_t n = int64_t(bands) * nlag;
+  const int64_t i = int64_t(blockIdx.x) * kMeanOuts + o;  // i = lag * bands + band
   double s = 0.0;
-  for (int64_t c = 0; c < clips; ++c) s += per_clip[(size_t(c) * nlag + lag) * bands + b];
-  corr[i] = s / double(clips);
+  if (i < n)
+    for (int64_t c = g; c < clips; c += kMeanGroups) s += per_clip[size_t(c) * size_t(n) + size_t(i)];
+  part[g][o] = s;
+  __syncthreads();
+  if (g == 0 && i < n) {
+    double t = 0.0;
+    for (int k = 0; k < kMeanGroups; ++k) t += part[k][o];
+    const int lag = int(i / bands), b = int(i % bands);
+    corr[size_t(b) * nlag + lag] = t / double(clips);
+  }
 }
 
 bool spec_args_ok(int64_t clips, int64_t frames, int32_t height, int32_t width, int32_t bands, int64_t max_lag) {
@@ -246,8 +586,8 @@ bool spec_args_ok(int64_t clips, int64_t frames, int32_t height, int32_t width, 
   if (max_lag < 0 || max_lag >= frames || max_lag + 1 > kSpecMaxLags) return false;
   if (height < 1 || width < 1 || height > 1024 || width > 1024) return false;
   if (int64_t(height) * width > 40960) return false;
-  if (dct_lds_bytes(height, width) > size_t(kSpecLdsBytes)) return false;
   if (bands < 1 || bands > kSpecMaxBands) return false;
+  if (!fused_fits(height, width, bands) && dct_lds_bytes(height, width) > size_t(kSpecLdsBytes)) return false;
   return true;
 }
 
@@ -261,7 +601,8 @@ int fademem_spectral_workspace_bytes(int64_t clips, int64_t frames, int32_t heig
                                      int64_t max_lag, size_t* bytes) {
   if (!bytes || !spec_args_ok(clips, frames, height, width, bands, max_lag)) return FADEMEM_EINVAL;
   SpecLayout L;
-  if (!spec_layout(clips, max_lag + 1, height, width, bands, &L)) return FADEMEM_EINVAL;
+  if (!spec_layout(clips, max_lag + 1, height, width, bands, fused_fits(height, width, bands), &L))
+    return FADEMEM_EINVAL;
   *bytes = L.total;
   return FADEMEM_OK;
 }
@@ -274,8 +615,9 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
     return FADEMEM_EINVAL;
   if (!spec_args_ok(clips, frames, height, width, bands, max_lag)) return FADEMEM_EINVAL;
   const int nlag = int(max_lag + 1);
+  const bool fused = fused_fits(height, width, bands);
   SpecLayout L;
-  if (!spec_layout(clips, nlag, height, width, bands, &L)) return FADEMEM_EINVAL;
+  if (!spec_layout(clips, nlag, height, width, bands, fused, &L)) return FADEMEM_EINVAL;
   if (workspace_bytes < L.total) return FADEMEM_ENOMEM;
   char* ws = static_cast<char*>(workspace);
   float* ah = reinterpret_cast<float*>(ws + L.off_ah);
@@ -290,20 +632,37 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
   hipLaunchKernelGGL(dct_basis_kernel, dim3((height * height + 255) / 256), dim3(256), 0, s, ah, int(height));
   hipLaunchKernelGGL(dct_basis_kernel, dim3((width * width + 255) / 256), dim3(256), 0, s, aw, int(width));
   hipLaunchKernelGGL(band_order_kernel, dim3(1), dim3(kOrderThreads), 0, s, band_of, HW, int(bands), perm, start);
-  const size_t lds = dct_lds_bytes(height, width);
-  if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(dct2_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-    if (e != hipSuccess) return FADEMEM_EHIP;
+  if (fused) {
+    const int lds = fused_lds(height, width, bands).total;
+    const FusedKernel fn = fused_kernel(height, width);
+    if (lds > 64 * 1024 &&
+        hipFuncSetAttribute(reinterpret_cast<const void*>(fn), hipFuncAttributeMaxDynamicSharedMemorySize, lds) !=
+            hipSuccess)
+      return FADEMEM_EHIP;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+      return FADEMEM_EHIP;
+    const int64_t total = clips * int64_t(nlag);
+    const unsigned grid = unsigned(total < cus ? total : cus);  // one block per CU, every block has a frame
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(kFusedThreads), size_t(lds), s, latents, frames, nlag, clips,
+                       int(height), int(width), ah, aw, perm, start, int(bands), per_clip);
+  } else {
+    const size_t lds = dct_lds_bytes(height, width);
+    if (lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(dct2_kernel),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return FADEMEM_EHIP;
+    }
+    const unsigned runs = unsigned((nlag + kDctFramesPerBlock - 1) / kDctFramesPerBlock);
+    hipLaunchKernelGGL(dct2_kernel, dim3(unsigned(clips), runs), dim3(kDctThreads), lds, s, latents, frames, nlag,
+                       int(height), int(width), ah, aw, d);
+    hipLaunchKernelGGL(band_corr_kernel, dim3(unsigned(clips), unsigned(nlag)), dim3(256), 0, s, d, nlag, HW, perm,
+                       start, int(bands), per_clip);
   }
-  const unsigned runs = unsigned((nlag + kDctFramesPerBlock - 1) / kDctFramesPerBlock);
-  hipLaunchKernelGGL(dct2_kernel, dim3(unsigned(clips), runs), dim3(kDctThreads), lds, s, latents, frames, nlag,
-                     int(height), int(width), ah, aw, d);
-  hipLaunchKernelGGL(band_corr_kernel, dim3(unsigned(clips), unsigned(nlag)), dim3(256), 0, s, d, nlag, HW, perm,
-                     start, int(bands), per_clip);
   const int64_t outs = int64_t(bands) * nlag;
-  hipLaunchKernelGGL(clip_mean_kernel, dim3(unsigned((outs + 255) / 256)), dim3(256), 0, s, per_clip, clips, nlag,
-                     int(bands), corr);
+  hipLaunchKernelGGL(clip_mean_kernel, dim3(unsigned((outs + kMeanOuts - 1) / kMeanOuts)),
+                     dim3(kMeanOuts * kMeanGroups), 0, s, per_clip, clips, nlag, int(bands), corr);
   return hipGetLastError() == hipSuccess ? FADEMEM_OK : FADEMEM_EHIP;
 }
 

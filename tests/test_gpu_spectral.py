@@ -27,8 +27,17 @@ def gpu_corr(lat_np, band_np, bands, max_lag):
     return sp.spectral_corr(lat, band, bands, max_lag).cpu().numpy()
 
 
-@pytest.mark.parametrize("clips,frames,H,W,bands,max_lag", [(3, 12, 20, 36, 8, 11), (1, 5, 7, 9, 3, 2),
-                                                             (2, 6, 96, 100, 16, 5), (4, 9, 60, 104, 24, 0)])
+# Frames up to 64 x 128 take the fused matrix-core kernel (1 to 4 tiles of 16
+# rows); larger ones the general two-kernel path.
+@pytest.mark.parametrize("clips,frames,H,W,bands,max_lag", [
+    (3, 12, 20, 36, 8, 11),      # fused, 2 row tiles, ragged columns
+    (1, 5, 7, 9, 3, 2),          # fused, 1 row tile
+    (2, 10, 40, 64, 12, 9),      # fused, 3 row tiles, full column tiles
+    (4, 9, 60, 104, 24, 0),      # fused, the paper's latent shape, lag 0 only
+    (5, 13, 64, 128, 16, 12),    # fused, largest shape
+    (2, 6, 96, 100, 16, 5),      # general path (rows > 64)
+    (2, 7, 40, 130, 10, 6),      # general path (columns > 128)
+])
 def test_spectral_parity_random(clips, frames, H, W, bands, max_lag):
     print(f"spectral clips={clips} frames={frames} H={H} W={W} bands={bands} max_lag={max_lag}", flush=True)
     lat = np.random.default_rng(H * W + frames).standard_normal((clips, frames, H, W)).astype(np.float32)
@@ -37,6 +46,25 @@ def test_spectral_parity_random(clips, frames, H, W, bands, max_lag):
     ref = oracle.band_correlations(lat, band, bands, max_lag)
     assert np.abs(got - ref).max() <= CORR_ABS, np.abs(got - ref).max()
     np.testing.assert_allclose(got[:, 0], 1.0, atol=1e-9)
+
+
+@pytest.mark.parametrize("H,W,bands", [(64, 128, 1024), (60, 104, 300)])
+def test_spectral_many_bands_with_empty_ones(H, W, bands):
+    """Fine partitions leave bands with fewer than two coefficients: their
+    coefficient is NaN on both sides; every other one within the bar."""
+    print(f"spectral many bands H={H} W={W} bands={bands}", flush=True)
+    lat = np.random.default_rng(bands).standard_normal((3, 5, H, W)).astype(np.float32)
+    band, _ = oracle.radial_band_of(H, W, bands)
+    got = gpu_corr(lat, band, bands, 4)
+    with np.errstate(invalid="ignore", divide="ignore"):
+        import warnings
+        with warnings.catch_warnings():
+            warnings.simplefilter("ignore")
+            ref = oracle.band_correlations(lat, band, bands, 4)
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert ok.sum() > 0
+    assert np.abs(got[ok] - ref[ok]).max() <= CORR_ABS
 
 
 def test_spectral_band_map_with_left_out_coefficients():
