@@ -218,11 +218,14 @@ int fademem_merge_counts(fademem_cache* cache, int64_t* total, int64_t* anchor, 
  * band_of: device [height][width] int32, the band of DCT coefficient
  * (u, v) (any value outside [0, bands) leaves the coefficient out).
  * workspace: device, 256-byte aligned, at least
- * fademem_spectral_workspace_bytes (it holds the DCT of the analysed
- * frames).  Limits: height*width <= 40960 and the frame, its transform and
- * both DCT bases within 160 KiB of LDS (e.g. 60 x 104); max_lag < frames,
- * max_lag < 65535; 1 <= bands <= 1024.  Asynchronous on `stream`.  A band
- * whose coefficients do not vary gets NaN.
+ * fademem_spectral_workspace_bytes (the DCT bases, the band order and the
+ * per-clip coefficients; frames of up to 64 x 128 are transformed on chip,
+ * larger ones also keep the DCT of the analysed frames there).  Limits:
+ * height*width <= 40960 and, above 64 x 128, the frame, its transform and
+ * both DCT bases within 160 KiB of LDS; max_lag < frames, max_lag < 65535;
+ * 1 <= bands <= 1024.  Asynchronous on `stream`; the library allocates
+ * nothing.  Every call with the same inputs gives the same bits.  A band
+ * whose coefficients do not vary, or that holds none, gets NaN.
  * Errors: EINVAL (NULL/misaligned pointers, sizes out of range), ENOMEM
  * (workspace too small), EHIP. */
 int fademem_spectral_workspace_bytes(int64_t clips, int64_t frames, int32_t height, int32_t width,

@@ -121,3 +121,29 @@ def test_spectral_argument_errors():
                         ctypes.c_void_p(ws.data_ptr()), wsb, ctypes.c_void_p(corr.data_ptr()), None)
     assert L.fademem_spectral_corr(*args(need - 1)) == fm.FADEMEM_ENOMEM
     assert L.fademem_spectral_corr(None, 2, 5, 8, 8, None, 4, 2, None, need, None, None) == fm.FADEMEM_EINVAL
+
+
+def test_spectral_full_workload_and_determinism():
+    """The benchmark's workload: 374 clips (32 distinct seeded clips, cycled)
+    of 177 latent frames at 60 x 104, 24 bands, every lag.  The clip mean is
+    linear, so the oracle's per-clip curves of the 32 distinct clips,
+    weighted by how often each occurs, give the expected mean exactly; every
+    C_k(lag) is checked.  Two calls give the same bits."""
+    import torch
+    from paper_2606_10671_amd import spectral as sp
+    C, T, H, W, K, distinct = 374, 177, 60, 104, 24, 32
+    print(f"spectral full workload clips={C} T={T} {H}x{W} bands={K}", flush=True)
+    gen = SpectralClips(0, T, H, W)  # host generator (seconds), then one copy to the device
+    clips = [gen.clip() for _ in range(distinct)]
+    lat = torch.stack([clips[c % distinct] for c in range(C)]).cuda().contiguous()
+    band_np, _ = sp.radial_band_map(H, W, K)
+    band = torch.from_numpy(band_np).cuda()
+    got = sp.spectral_corr(lat, band, K, T - 1).cpu().numpy()
+    again = sp.spectral_corr(lat, band, K, T - 1).cpu().numpy()
+    assert np.array_equal(got.view(np.uint64), again.view(np.uint64))
+    counts = np.bincount(np.arange(C) % distinct, minlength=distinct)
+    ref = np.zeros((K, T))
+    for d in range(distinct):
+        ref += counts[d] * oracle.band_correlations(clips[d].cpu().numpy()[None], band_np, K, T - 1)
+    ref /= C
+    assert np.abs(got - ref).max() <= CORR_ABS, np.abs(got - ref).max()
