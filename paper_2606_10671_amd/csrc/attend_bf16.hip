@@ -6,8 +6,9 @@
 // Sec. 4.1: the chunk attends over the memory entries plus its own frames).
 //
 // Design (workgroup = 8 waves x 32 queries of one head, one workgroup per
-// CU, two waves per SIMD; every value stays in the 256 architectural VGPRs
-// of a wave):
+// CU, two waves per SIMD; the steady-state loop keeps every value in the 256
+// architectural VGPRs of a wave, while the last tiles and the epilogue
+// spill):
 // * The 256 queries of a workgroup share each K/V tile, which is streamed
 //   from L2 into LDS once for all of them.
 // * Transposed scores: S^T = K Q^T puts 16 keys of ONE query in each
