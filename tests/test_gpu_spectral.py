@@ -147,3 +147,36 @@ def test_spectral_full_workload_and_determinism():
         ref += counts[d] * oracle.band_correlations(clips[d].cpu().numpy()[None], band_np, K, T - 1)
     ref /= C
     assert np.abs(got - ref).max() <= CORR_ABS, np.abs(got - ref).max()
+
+
+@pytest.mark.parametrize("clips,frames,H,W,bands,max_lag", [(3, 7, 60, 104, 40, 6), (2, 5, 70, 90, 12, 4)])
+def test_spectral_arbitrary_band_map(clips, frames, H, W, bands, max_lag):
+    """Bands need not be radial: a random assignment (some bands empty,
+    some coefficients left out), on the fused (60 x 104) and the general
+    (70 x 90) path."""
+    print(f"spectral random bands {H}x{W} bands={bands}", flush=True)
+    rng = np.random.default_rng(bands)
+    lat = rng.standard_normal((clips, frames, H, W)).astype(np.float32)
+    band = rng.integers(-1, bands - 3, (H, W)).astype(np.int32)  # the last three bands stay empty
+    got = gpu_corr(lat, band, bands, max_lag)
+    import warnings
+    with np.errstate(invalid="ignore", divide="ignore"), warnings.catch_warnings():
+        warnings.simplefilter("ignore")
+        ref = oracle.band_correlations(lat, band, bands, max_lag)
+    assert np.array_equal(np.isnan(got), np.isnan(ref)) and np.isnan(got[-3:]).all()
+    ok = ~np.isnan(ref)
+    assert np.abs(got[ok] - ref[ok]).max() <= CORR_ABS
+
+
+@pytest.mark.parametrize("clips,frames,H,W,bands,max_lag", [(1, 1, 1, 1, 1, 0), (2, 1, 16, 16, 4, 0)])
+def test_spectral_degenerate(clips, frames, H, W, bands, max_lag):
+    """One frame (lag 0 only); a 1 x 1 frame whose single coefficient forms
+    the only band: a band of one coefficient has no spread, so NaN."""
+    lat = np.random.default_rng(H).standard_normal((clips, frames, H, W)).astype(np.float32)
+    band = np.zeros((1, 1), np.int32) if H * W == 1 else oracle.radial_band_of(H, W, bands)[0]
+    got = gpu_corr(lat, band, bands, max_lag)
+    assert got.shape == (bands, 1)
+    if H * W == 1:
+        assert np.isnan(got).all()
+    else:
+        np.testing.assert_allclose(got, 1.0, atol=1e-9)
