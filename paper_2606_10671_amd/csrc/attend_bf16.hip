@@ -55,8 +55,9 @@ namespace fademem {
 // group i (i < rem) and its tail [head_len, tiles) to group
 // rem + i / tails_per: the G - rem tail groups each take tails_per
 // consecutive tails.  head_len = tiles - tail_len, tail_len =
-// tiles / (tails_per + 1), so a tail group's tails_per tails are no more
-// work than one head part.  Every group starts its parts at the same key
+// (tiles - o (tails_per - 1)) / (tails_per + 1) with o = kSegOverhead key
+// tiles per extra segment, so a tail group's tails_per tails, with their
+// segment overheads, are no more work than one head part.  Every group starts its parts at the same key
 // tile at the same time, so the groups of one XCD read the same K/V tiles
 // together and those come from its L2.  A split tile leaves its head part
 // in scratch slot i and its tail in slot rem + i; a second kernel merges
@@ -91,6 +92,7 @@ constexpr int kBN = 64;            // keys per tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleBound = 256.0f;  // redo a tile whose weights exceed 2^8
+constexpr int kSegOverhead = 2;          // key tiles' worth of time a segment's prologue and epilogue cost
 static_assert(QB * 32 == kQW && (QB == 1 || QB == 2), "32-query blocks per wave");
 
 template <int D>
@@ -828,7 +830,13 @@ hipError_t launch_d(AttnKernel kernel, AttnKernel merge, std::once_flag& attr_on
   plan.rounds = total / plan.groups;
   plan.rem = total - plan.rounds * plan.groups;
   plan.tails_per = plan.rem > 0 ? (plan.rem + (plan.groups - plan.rem) - 1) / (plan.groups - plan.rem) : 1;
-  plan.tail_len = plan.tiles / (plan.tails_per + 1);
+  {
+    // A tail group runs tails_per segments, each with a prologue (two tile
+    // loads waited in full) and an epilogue: about kSegOverhead key tiles
+    // each, beyond the head part's one.
+    const int over = kSegOverhead * (plan.tails_per - 1);
+    plan.tail_len = plan.tiles > over ? (plan.tiles - over) / (plan.tails_per + 1) : 0;
+  }
   plan.head_len = plan.tiles - plan.tail_len;
   const int launched =
       plan.rounds > 0 ? plan.groups
