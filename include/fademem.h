@@ -219,7 +219,7 @@ int fademem_merge_counts(fademem_cache* cache, int64_t* total, int64_t* anchor, 
  * (u, v) (any value outside [0, bands) leaves the coefficient out).
  * workspace: device, 256-byte aligned, at least
  * fademem_spectral_workspace_bytes (the DCT bases, the band order and the
- * per-clip coefficients; frames of up to 64 x 128 are transformed on chip,
+ * per-clip band sums; frames of up to 64 x 128 are transformed on chip,
  * larger ones also keep the DCT of the analysed frames there).  Limits:
  * height*width <= 40960 and, above 64 x 128, the frame, its transform and
  * both DCT bases within 160 KiB of LDS; max_lag < frames, max_lag < 65535;

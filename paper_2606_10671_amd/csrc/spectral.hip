@@ -16,11 +16,12 @@
 //   T = z A_W^T and D = A_H T on the fp32 matrix cores
 //   (v_mfma_f32_16x16x4_f32; wave j owns the 16 columns v of tile j), the
 //   second product taking T straight from the first one's accumulators,
-//   then D written to LDS in band order and reduced per band (fp64 sums)
-//   against frame 0's coefficients (kept in LDS) to the Pearson
-//   coefficient; no transform ever reaches HBM;
-// * clip_mean_kernel -- the mean over clips, in a fixed order (every call
-//   gives the same bits).
+//   then D written to LDS in band order and reduced per band to the fp64
+//   sums S_y, S_yy and S_xy against frame 0's coefficients x (kept in LDS);
+//   no transform ever reaches HBM;
+// * clip_mean_kernel -- per clip the Pearson coefficient from those sums
+//   (frame 0's own, at lag 0, give S_x and S_xx), then the mean over clips
+//   in a fixed order (every call gives the same bits).
 // Larger frames take the general path:
 // * dct2_kernel -- one block per (clip, run of frames): both bases (as
 //   transposes) in LDS once, then per frame z^T in LDS, T = z A_W^T and
@@ -28,9 +29,8 @@
 //   reads (8 FMAs per read); fp32 products and sums; sizes padded to
 //   multiples of 4 with zeros;
 // * band_corr_kernel -- one block per (clip, lag): each wave takes bands in
-//   turn, sums x, y, x^2, y^2, xy over the band in fp64 (lanes, then a wave
-//   reduction), and writes the Pearson coefficient
-//   (n Sxy - Sx Sy) / sqrt((n Sxx - Sx^2)(n Syy - Sy^2)).
+//   turn and sums y, y^2 and x y over the band in fp64 (lanes, then a wave
+//   reduction), x being frame 0.
 #include <math.h>
 #include <string.h>
 
@@ -50,7 +50,7 @@ struct SpecLayout {
 
 bool spec_layout(int64_t clips, int64_t nlag, int64_t H, int64_t W, int64_t bands, bool fused, SpecLayout* L) {
   const double d_bytes = fused ? 0.0 : double(clips) * double(nlag) * double(H) * double(W) * 4.0;
-  const double c_bytes = double(clips) * double(nlag) * double(bands) * 8.0;
+  const double c_bytes = double(clips) * double(nlag) * double(bands) * 24.0;
   if (d_bytes > 1e15 || c_bytes > 1e15) return false;
   size_t off = 0;
   L->off_ah = off;    off = rup(off + size_t(H * H) * 4);
@@ -58,7 +58,7 @@ bool spec_layout(int64_t clips, int64_t nlag, int64_t H, int64_t W, int64_t band
   L->off_d = off;     off = rup(off + (fused ? 0 : size_t(clips) * size_t(nlag) * size_t(H * W) * 4));
   L->off_perm = off;  off = rup(off + size_t(H * W) * 4);
   L->off_start = off; off = rup(off + size_t(bands + 1) * 4);
-  L->off_clip = off;  off = rup(off + size_t(clips) * size_t(nlag) * size_t(bands) * 8);
+  L->off_clip = off;  off = rup(off + size_t(clips) * size_t(nlag) * size_t(bands) * 24);
   L->total = off;
   return true;
 }
@@ -222,29 +222,24 @@ __global__ __launch_bounds__(256) void band_corr_kernel(const float* D, int nlag
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* x = D + size_t(c) * size_t(nlag) * size_t(HW);
   const float* y = x + size_t(lag) * size_t(HW);
-  double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(lag)) * size_t(bands);
+  double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(lag)) * size_t(bands) * 3;
   for (int b = wave; b < bands; b += 4) {
     const int s0 = start[b], s1 = start[b + 1];
-    double sx = 0, sy = 0, sxx = 0, syy = 0, sxy = 0;
+    double sy = 0, syy = 0, sxy = 0;
     for (int j = s0 + lane; j < s1; j += 64) {
       const int i = perm[j];
       const double xv = x[i], yv = y[i];
-      sx += xv;
       sy += yv;
-      sxx += xv * xv;
       syy += yv * yv;
       sxy += xv * yv;
     }
-    sx = wave_sum(sx);
     sy = wave_sum(sy);
-    sxx = wave_sum(sxx);
     syy = wave_sum(syy);
     sxy = wave_sum(sxy);
     if (lane == 0) {
-      const double n = double(s1 - s0);
-      const double cov = n * sxy - sx * sy;
-      const double vx = n * sxx - sx * sx, vy = n * syy - sy * sy;
-      out[b] = cov / sqrt(vx * vy);  // NaN for a band without spread
+      out[3 * b] = sy;
+      out[3 * b + 1] = syy;
+      out[3 * b + 2] = sxy;
     }
   }
 }
@@ -261,10 +256,9 @@ __host__ __device__ inline int r16(int x) { return (x + 15) / 16 * 16; }
 // 16-byte reads of 16 consecutive rows fall in distinct banks; dl: the
 // transform D in band order (at set-up, the inverse of the band order);
 // xl: frame 0's coefficients in band order; ahl: A_H as the second
-// product's A fragments; sl: the band starts; sxl: per band, frame 0's sum
-// and sum of squares.
+// product's A fragments; sl: the band starts.
 struct FusedLds {
-  int zl, dl, xl, ahl, sl, sxl, total;
+  int zl, dl, xl, ahl, sl, total;
 };
 __host__ __device__ inline FusedLds fused_lds(int H, int W, int bands) {
   const int HT = (H + 15) / 16;
@@ -275,7 +269,6 @@ __host__ __device__ inline FusedLds fused_lds(int H, int W, int bands) {
   L.xl = off;  off += r16(H * W * 4);
   L.ahl = off; off += r16(HT * HT * 256 * 4);
   L.sl = off;  off += r16((bands + 1) * 4);
-  L.sxl = off; off += r16(bands * 16);
   L.total = off;
   return L;
 }
@@ -319,8 +312,7 @@ __device__ __forceinline__ double wave_total(double v) {
 //   product from its accumulators with no data movement.
 // Each lane writes its D values straight to their band-order positions, so
 // a band is a contiguous run of dl and xl.  Band b is always reduced by wave
-// b % 8, which also keeps frame 0's run and sums for it: those need no
-// barrier.
+// b % 8, which also keeps frame 0's run for it: that needs no barrier.
 template <int HT, int NQ>
 __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const float* latents, int64_t frames, int nlag,
                                                                        int64_t clips, int H, int W, const float* AH,
@@ -335,7 +327,6 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
   float* xl = reinterpret_cast<float*>(smem + L.xl);
   float* ahl = reinterpret_cast<float*>(smem + L.ahl);
   int32_t* sl = reinterpret_cast<int32_t*>(smem + L.sl);
-  double* sxl = reinterpret_cast<double*>(smem + L.sxl);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int S = fused_zl_stride(W);  // NQ = (W + 15) / 16 quads of 16 columns = v-tiles
   const int HW = H * W;
@@ -482,10 +473,10 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
     }
     if (more) store_z();
     __syncthreads();
-    double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(t)) * size_t(bands);
+    double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(t)) * size_t(bands) * 3;
     for (int b = wave; b < bands; b += kFusedThreads / 64) {
       const int s0 = sl[b], s1 = sl[b + 1];
-      double sx, sxx, sy = 0, syy = 0, sxy = 0;
+      double sy = 0, syy = 0, sxy = 0;
       if (t == 0) {  // frame 0 of a clip: its run becomes x
         for (int j = s0 + lane; j < s1; j += 64) {
           const float yf = dl[j];
@@ -496,13 +487,7 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
         }
         sy = wave_total(sy);
         syy = wave_total(syy);
-        sx = sy;
-        sxx = syy;
         sxy = syy;
-        if (lane == 0) {
-          sxl[2 * b] = sx;
-          sxl[2 * b + 1] = sxx;
-        }
       } else {
         int j = s0 + lane;
         for (; j + 192 < s1; j += 256) {  // four elements per lane in flight
@@ -529,14 +514,11 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
         sy = wave_total(sy);
         syy = wave_total(syy);
         sxy = wave_total(sxy);
-        sx = sxl[2 * b];
-        sxx = sxl[2 * b + 1];
       }
       if (emit && lane == 0) {
-        const double n = double(s1 - s0);
-        const double cov = n * sxy - sx * sy;
-        const double vx = n * sxx - sx * sx, vy = n * syy - sy * sy;
-        out[b] = cov / sqrt(vx * vy);  // NaN for a band without spread
+        out[3 * b] = sy;
+        out[3 * b + 1] = syy;
+        out[3 * b + 2] = sxy;
       }
     }
     c = cn;
@@ -557,23 +539,39 @@ FusedKernel fused_kernel(int H, int W) {  // H <= 64, W <= 128
   return HT == 1 ? kFusedRow<1>[q] : HT == 2 ? kFusedRow<2>[q] : HT == 3 ? kFusedRow<3>[q] : kFusedRow<4>[q];
 }
 
-// Mean over clips of per_clip[clip][lag][band] into corr[band][lag].  Block
-// = 16 consecutive (lag, band) outputs x 16 clip groups: group g sums clips
-// g, g + 16, ... in order, then the 16 partial sums are added in group order
-// (a fixed order, so every call gives the same bits).
+// Per clip, band b and lag, the Pearson coefficient from the band sums
+// S_y, S_yy, S_xy of frame lag (x = frame 0, whose own sums at lag 0 are
+// S_x, S_xx):
+//   r = (n S_xy - S_x S_y) / sqrt((n S_xx - S_x^2)(n S_yy - S_y^2)),
+// NaN for a band without spread; then the mean over clips into
+// corr[band][lag].  Block = 16 consecutive (lag, band) outputs x 16 clip
+// groups: group g takes clips g, g + 16, ... in order, then the 16 partial
+// sums are added in group order (a fixed order, so every call gives the
+// same bits).
 constexpr int kMeanOuts = 16, kMeanGroups = 16;
-__global__ __launch_bounds__(kMeanOuts * kMeanGroups) void clip_mean_kernel(const double* per_clip, int64_t clips,
+__global__ __launch_bounds__(kMeanOuts * kMeanGroups) void clip_mean_kernel(const double* per_clip,
+                                                                           const int32_t* start, int64_t clips,
                                                                            int nlag, int bands, double* corr) {
   __shared__ double part[kMeanGroups][kMeanOuts];
   const int o = threadIdx.x % kMeanOuts, g = threadIdx.x / kMeanOuts;
-  const int64_t n = int64_t(bands) * nlag;
+  const int64_t n_out = int64_t(bands) * nlag;
   const int64_t i = int64_t(blockIdx.x) * kMeanOuts + o;  // i = lag * bands + band
   double s = 0.0;
-  if (i < n)
-    for (int64_t c = g; c < clips; c += kMeanGroups) s += per_clip[size_t(c) * size_t(n) + size_t(i)];
+  if (i < n_out) {
+    const int b = int(i % bands);
+    const double n = double(start[b + 1] - start[b]);
+    for (int64_t c = g; c < clips; c += kMeanGroups) {
+      const double* f = per_clip + (size_t(c) * size_t(n_out) + size_t(i)) * 3;
+      const double* f0 = per_clip + (size_t(c) * size_t(n_out) + size_t(b)) * 3;  // lag 0
+      const double sx = f0[0], sxx = f0[1], sy = f[0], syy = f[1], sxy = f[2];
+      const double cov = n * sxy - sx * sy;
+      const double vx = n * sxx - sx * sx, vy = n * syy - sy * sy;
+      s += cov / sqrt(vx * vy);
+    }
+  }
   part[g][o] = s;
   __syncthreads();
-  if (g == 0 && i < n) {
+  if (g == 0 && i < n_out) {
     double t = 0.0;
     for (int k = 0; k < kMeanGroups; ++k) t += part[k][o];
     const int lag = int(i / bands), b = int(i % bands);
@@ -662,7 +660,7 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
   }
   const int64_t outs = int64_t(bands) * nlag;
   hipLaunchKernelGGL(clip_mean_kernel, dim3(unsigned((outs + kMeanOuts - 1) / kMeanOuts)),
-                     dim3(kMeanOuts * kMeanGroups), 0, s, per_clip, clips, nlag, int(bands), corr);
+                     dim3(kMeanOuts * kMeanGroups), 0, s, per_clip, start, clips, nlag, int(bands), corr);
   return hipGetLastError() == hipSuccess ? FADEMEM_OK : FADEMEM_EHIP;
 }
 
