@@ -50,18 +50,29 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 ATTN_TRAFFIC = {"source_sha256": "1f336d442f3be6c1", "workload": "wan1.3b-1layer", "bytes_per_call": 760845833}
 
 
-def attn_traffic(workload):
-    """Measured HBM bytes per attention call, or None if the kernel source
+# HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.
+SPEC_TRAFFIC = {"source_sha256": "461a69cad4bcc98c", "workload": "spectral-374clips", "bytes_per_call": 1740060589}
+
+
+def measured_traffic(table, source, workload):
+    """Measured HBM bytes per call from `table`, or None if the kernel source
     changed since the counters were taken or the workload differs."""
     import hashlib
-    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_10671_amd", "csrc", "attend_bf16.hip")
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_10671_amd", "csrc", source)
     try:
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        with open(src, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
     except OSError:
         return None
-    if sha != ATTN_TRAFFIC["source_sha256"] or workload != ATTN_TRAFFIC["workload"]:
+    if sha != table["source_sha256"] or workload != table["workload"]:
         return None
-    return ATTN_TRAFFIC["bytes_per_call"]
+    return table["bytes_per_call"]
+
+
+def attn_traffic(workload):
+    """Measured HBM bytes per attention call (None: source or workload differ)."""
+    return measured_traffic(ATTN_TRAFFIC, "attend_bf16.hip", workload)
 
 
 def parse():
@@ -191,7 +202,9 @@ def run_spectral(args):
         "fit": {"a": a, "b": b, "horizons": h.tolist()},
         "roofline": {"bound": "mfma", "kernel": "whole call (spectral_fused_kernel dominates)",
                      "achieved": round(tflops, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None},
+                     "frac": round(tflops / FP32_MFMA_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(SPEC_TRAFFIC, "spectral.hip", args.workload),
+                     "traffic_unit": "bytes per call (HBM read + write)"},
     }
     if not args.no_cpu_baseline:
         import oracle

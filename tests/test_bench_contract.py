@@ -39,3 +39,9 @@ def test_workloads_at_the_configured_sizes(name, blk, flop):
 ])
 def test_fused_update_block_count(js, count0, F, M, anchor, op, expect):
     assert bench.fused_block_ios(js, count0, F, M, anchor, op) == expect
+
+
+def test_measured_traffic_is_tied_to_its_workload():
+    assert bench.attn_traffic("wan14b-1layer") is None
+    assert bench.measured_traffic(bench.SPEC_TRAFFIC, "spectral.hip", "wan1.3b-1layer") is None
+    assert bench.measured_traffic(bench.ATTN_TRAFFIC, "no_such_file.hip", "wan1.3b-1layer") is None
