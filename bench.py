@@ -422,7 +422,8 @@ def main():
         "roofline": {
             "bound": "mfma" if is_bf16 else "alu",
             "kernel": ("attend_bf16_d128 + attend_bf16_merge_d128 (one attend call)" if D == 128 else
-                       "attend_bf16_d64 + attend_bf16_merge_d64 (one attend call)") if is_bf16 else "attend_f32_kernel",
+                       "attend_bf16_d64 + attend_bf16_merge_d64 (one attend call)") if is_bf16
+                      else "attend_f32_kernel + attend_f32_combine_kernel (one attend call)",
             "achieved": round(attn_tflops, 2),
             "peak": peak,
             "unit": "TFLOP/s",

@@ -761,7 +761,7 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
   L.blk_bytes = size_t(cfg->tokens_per_block) * L.row_elems * L.elt;
   L.blk_stride = round_up(L.blk_bytes, 256);
   L.off_ws = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
-  L.ws_bytes = cfg->dtype == FADEMEM_BF16 ? attend_ws_bytes(cfg->head_dim) : 0;
+  L.ws_bytes = cfg->dtype == FADEMEM_BF16 ? attend_ws_bytes(cfg->head_dim) : f32_ws_bytes(cfg->head_dim);
   L.off_view = round_up(L.off_ws + L.ws_bytes, 256);
   L.view_bytes = cfg->rope_pairs > 0 ? size_t(cfg->budget) * 2 * L.blk_stride + round_up(4 * size_t(cfg->budget), 256)
                                      : 0;

@@ -36,6 +36,20 @@ __host__ __device__ constexpr size_t attend_ws_bytes(int head_dim) {
   return 2 * size_t(kSkMaxGroups) * attend_slot_floats(head_dim) * sizeof(float);
 }
 
+// fp32 attention work split: a workgroup takes kF32Queries queries of one
+// head over a range of key tiles; when the key axis is cut into several
+// ranges, each leaves its partial result (unnormalised O, row max and row
+// sum per query) in a slot and a second kernel combines them.  At most
+// kF32MaxParts slots per call.
+constexpr int kF32Queries = 64;
+constexpr int kF32MaxParts = 512;
+__host__ __device__ constexpr size_t f32_part_floats(int head_dim) {
+  return size_t(kF32Queries) * size_t(head_dim + 2);
+}
+__host__ __device__ constexpr size_t f32_ws_bytes(int head_dim) {
+  return size_t(kF32MaxParts) * f32_part_floats(head_dim) * sizeof(float);
+}
+
 // Device-resident header at the start of the pool.  Written only by the
 // library's kernels; the host reads it back for merge_log.
 struct DevHeader {
@@ -78,8 +92,8 @@ struct Layout {
   size_t blk_bytes;       // N*H*D*elt: one K (or V) block
   size_t blk_stride;      // blk_bytes rounded up to 256
   size_t row_elems;       // H*D: elements per token row
-  size_t off_ws;          // attention scratch (bf16 caches), after the KV region
-  size_t ws_bytes;        // attend_ws_bytes(D) for bf16, 0 for fp32
+  size_t off_ws;          // attention scratch, after the KV region
+  size_t ws_bytes;        // attend_ws_bytes(D) for bf16, f32_ws_bytes(D) for fp32
   size_t off_view;        // RoPE view: M slots of K (rotated) and V, then an identity slot table
   size_t view_bytes;      // 0 when rope_pairs = 0
   size_t total;           // off_view + view_bytes
@@ -110,7 +124,7 @@ struct AttendArgs {
   int64_t q_tokens;
   size_t slot_stride;         // bytes between consecutive slots' K blocks (2*blk_stride)
   size_t v_offset;            // bytes from a slot's K block to its V block
-  float* ws;                  // attention scratch (bf16): 2*kSkMaxGroups slots
+  float* ws;                  // attention scratch: 2*kSkMaxGroups slots (bf16), kF32MaxParts slots (fp32)
   int heads;
   int head_dim;
   float scale;

@@ -50,7 +50,8 @@ def test_pool_bytes_layout():
     """Metadata (< 64 KiB) + (M+1) K and V slots per layer; bf16 caches add
     the attention's split-work scratch: two slots per workgroup (at most
     256) of 256 queries x D fp32 partial O plus 1024 fp32 maxima and sums
-    (the same bytes as 512 slots of 128 queries x D plus 256 floats)."""
+    (the same bytes as 512 slots of 128 queries x D plus 256 floats); fp32
+    caches add 512 slots of 64 queries x (D + 2) floats for key ranges."""
     n = fm.fademem_pool_bytes(fm.make_config(**GOOD))
     blk = 1560 * 12 * 128 * 2
     ws = 2 * 512 * (128 * 128 + 2 * 256) * 4
@@ -58,7 +59,7 @@ def test_pool_bytes_layout():
     n30 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "layers": 30}))
     assert n30 - n == 29 * 22 * 2 * blk
     nf = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "dtype": fm.FADEMEM_F32}))
-    assert nf - n == 22 * 2 * blk - ws
+    assert nf - n == 22 * 2 * blk - ws + 512 * 64 * (128 + 2) * 4
     n64 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "head_dim": 64}))
     assert n - n64 == 22 * blk + ws - 2 * 512 * (128 * 64 + 2 * 256) * 4
     # temporal RoPE handling adds the exposed copy of M entries' K and V
