@@ -411,6 +411,11 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
 
   DevHeader* hdr = reinterpret_cast<DevHeader*>(a.pool);
   int32_t* log = reinterpret_cast<int32_t*>(a.pool + a.lay.off_log);
+  int64_t merges = 0, anchors = 0;  // the header's counters, read once and written back at the end (thread 0)
+  if (tid == 0) {
+    merges = hdr->merges_total;
+    anchors = hdr->anchor_merges;
+  }
   int n = a.n0;
   for (int f = 0; f < a.frames; ++f) {
     const int64_t t = a.first_position + f;
@@ -452,10 +457,9 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
       span_s[j] = s_new;
       kind_s[j] = nk;
       idx_s[j] = ni;
-      const int64_t lk = hdr->merges_total;
-      log[lk % kLogCap] = j;
-      hdr->merges_total = lk + 1;
-      if (anchor_pair) hdr->anchor_merges += 1;
+      log[merges % kLogCap] = j;
+      merges += 1;
+      if (anchor_pair) anchors += 1;
     }
     __syncthreads();
     // Replace: entries j+2..n-1 move down by one.
@@ -508,6 +512,8 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
     }
     for (int i = n; i < slots; ++i) w.order[i] = free_s[next++];
     *reinterpret_cast<UpdatePlan*>(a.pool + a.lay.off_prog) = plan;
+    hdr->merges_total = merges;
+    hdr->anchor_merges = anchors;
   }
   for (int i = tid; i < n; i += 256) {
     w.first[i] = first_s[i];
