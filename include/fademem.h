@@ -109,7 +109,11 @@ typedef struct fademem_config {
 typedef struct fademem_cache fademem_cache; /* opaque host object */
 
 /* Bytes of device pool a configuration needs: (M+1) KV slots per layer for
- * K and V, plus the memory's metadata.  Returns EINVAL for a bad config. */
+ * K and V, the memory's metadata, the attention's scratch for split work
+ * (bf16: partial results of split query tiles, 69.2 MB at D = 128; fp32:
+ * partial results of key ranges, 512 x 64 x (D+2) floats) and, with
+ * rope_pairs > 0, the re-indexed view of M entries' K and V.  Returns
+ * EINVAL for a bad config. */
 int fademem_pool_bytes(const fademem_config* cfg, size_t* bytes);
 
 /* Create a cache over a caller-owned device pool of `pool_bytes` bytes
@@ -154,8 +158,9 @@ int fademem_consolidate(fademem_cache* cache, void* stream);
  * F sequential Alg. S1 updates that follow a chunk's final denoising step
  * (Sec. 4.1; supplementary Sec. S4: one entry per latent frame).  State,
  * merge log and every stored K/V bit equal those of `frames` calls of
- * fademem_insert + fademem_consolidate.  Each K/V block that changes is
- * written once (a chain of merges is evaluated in registers, each merge
+ * fademem_insert + fademem_consolidate.  Frames are taken in groups of up
+ * to four; within a group each K/V block that changes is written once (a
+ * chain of merges is evaluated in registers, each merge
  * rounded to the storage type as on its own), and frames that a merge of
  * the same call consumes are read from the caller's buffers, never copied
  * into the pool.  k[l], v[l] (host arrays of `layers` device pointers) are
