@@ -52,7 +52,7 @@ ATTN_TRAFFIC = {"source_sha256": "1f336d442f3be6c1", "workload": "wan1.3b-1layer
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.
-SPEC_TRAFFIC = {"source_sha256": "461a69cad4bcc98c", "workload": "spectral-374clips", "bytes_per_call": 1740060589}
+SPEC_TRAFFIC = {"source_sha256": "9ead68d6867c130d", "workload": "spectral-374clips", "bytes_per_call": 1740288092}
 
 
 def measured_traffic(table, source, workload):

@@ -17,8 +17,10 @@
 //   (v_mfma_f32_16x16x4_f32; wave j owns the 16 columns v of tile j), the
 //   second product taking T straight from the first one's accumulators,
 //   then D written to LDS in band order and reduced per band to the fp64
-//   sums S_y, S_yy and S_xy against frame 0's coefficients x (kept in LDS);
-//   no transform ever reaches HBM;
+//   sums S_y, S_yy and S_xy against frame 0's coefficients x (kept in LDS).
+//   Frames go in pairs: both transforms are staged, then one band pass
+//   sums both (six sums per band), so the band pass's latency is paid once
+//   per two frames; no transform ever reaches HBM;
 // * clip_mean_kernel -- per clip the Pearson coefficient from those sums
 //   (frame 0's own, at lag 0, give S_x and S_xx), then the mean over clips
 //   in a fixed order (every call gives the same bits).
@@ -255,10 +257,11 @@ __host__ __device__ inline int r16(int x) { return (x + 15) / 16 * 16; }
 // rows of stride S = 16 n + 4 floats (zero outside H x W), so that the
 // 16-byte reads of 16 consecutive rows fall in distinct banks; dl: the
 // transform D in band order (at set-up, the inverse of the band order);
+// dl2: the second frame of a pair;
 // xl: frame 0's coefficients in band order; ahl: A_H as the second
 // product's A fragments; sl: the band starts.
 struct FusedLds {
-  int zl, dl, xl, ahl, sl, total;
+  int zl, dl, dl2, xl, ahl, sl, total;
 };
 __host__ __device__ inline FusedLds fused_lds(int H, int W, int bands) {
   const int HT = (H + 15) / 16;
@@ -266,6 +269,7 @@ __host__ __device__ inline FusedLds fused_lds(int H, int W, int bands) {
   int off = 0;
   L.zl = off;  off += r16(16 * HT * fused_zl_stride(W) * 4);
   L.dl = off;  off += r16(H * W * 4 + 4);  // + a spare slot that takes left-out coefficients
+  L.dl2 = off; off += r16(H * W * 4 + 4);  // the second frame of a pair
   L.xl = off;  off += r16(H * W * 4);
   L.ahl = off; off += r16(HT * HT * 256 * 4);
   L.sl = off;  off += r16((bands + 1) * 4);
@@ -410,32 +414,21 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
       }
     }
   };
-  // current job (c, t); the first is frame 0 of c_first (no output) when the
-  // share starts past it
-  int64_t c = c_first;
-  int t = 0;
-  bool emit = t_first == 0;
-  load_z(c, t);
-  __syncthreads();  // every lane has read its positions from inv
-  store_z();
-  __syncthreads();
+  struct Job {
+    int64_t c;
+    int t;
+    bool emit;
+  };
+  auto next_job = [&](const Job& j) -> Job {
+    if (!j.emit) return Job{j.c, t_first, true};
+    return j.t + 1 == nlag ? Job{j.c + 1, 0, true} : Job{j.c, j.t + 1, true};
+  };
+  float* dl2 = reinterpret_cast<float*>(smem + L.dl2);
   auto zfrag = [&](f32x4* a, int q) {
 #pragma unroll
     for (int i = 0; i < HT; ++i)
       a[i] = *reinterpret_cast<const f32x4*>(zl + (16 * i + (lane & 15)) * S + 16 * q + 4 * (lane >> 4));
-  };
-  for (int64_t k = 0; k < njobs; ++k) {
-    const bool more = k + 1 < njobs;
-    int64_t cn = c;
-    int tn = t + 1;
-    if (!emit) {
-      tn = t_first;
-    } else if (tn == nlag) {
-      cn = c + 1;
-      tn = 0;
-    }
-    if (more) load_z(cn, tn);
-    f32x4 dacc[HT];
+  };  auto products = [&](f32x4 (&dacc)[HT]) {
     if (mma) {
       f32x4 tacc[HT], acur[HT];
 #pragma unroll
@@ -463,23 +456,26 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
             dacc[a] = __builtin_amdgcn_mfma_f32_16x16x4f32(ah[a][r], tacc[i][r], dacc[a], 0, 0, 0);
       }
     }
-    __syncthreads();  // every read of zl, and the previous frame's band sums, are done
+  };
+  auto scatter = [&](float* dst, const f32x4 (&dacc)[HT]) {
     if (mma) {
 #pragma unroll
       for (int a = 0; a < HT; ++a)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          dl[pos[4 * a + r]] = dacc[a][r];
+        for (int r = 0; r < 4; ++r) dst[pos[4 * a + r]] = dacc[a][r];
     }
-    if (more) store_z();
-    __syncthreads();
+  };
+  auto reduce1 = [&](const Job& jb, const float* dsrc) {
+    const int64_t c = jb.c;
+    const int t = jb.t;
+    const bool emit = jb.emit;
     double* out = per_clip + (size_t(c) * size_t(nlag) + size_t(t)) * size_t(bands) * 3;
     for (int b = wave; b < bands; b += kFusedThreads / 64) {
       const int s0 = sl[b], s1 = sl[b + 1];
       double sy = 0, syy = 0, sxy = 0;
       if (t == 0) {  // frame 0 of a clip: its run becomes x
         for (int j = s0 + lane; j < s1; j += 64) {
-          const float yf = dl[j];
+          const float yf = dsrc[j];
           xl[j] = yf;
           const double y = yf;
           sy += y;
@@ -495,7 +491,7 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
 #pragma unroll
           for (int m = 0; m < 4; ++m) {
             xf[m] = xl[j + 64 * m];
-            yf[m] = dl[j + 64 * m];
+            yf[m] = dsrc[j + 64 * m];
           }
 #pragma unroll
           for (int m = 0; m < 4; ++m) {
@@ -506,7 +502,7 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
           }
         }
         for (; j < s1; j += 64) {
-          const double x = xl[j], y = dl[j];
+          const double x = xl[j], y = dsrc[j];
           sy += y;
           syy = fma(y, y, syy);
           sxy = fma(x, y, sxy);
@@ -521,9 +517,90 @@ __global__ __launch_bounds__(kFusedThreads) void spectral_fused_kernel(const flo
         out[3 * b + 2] = sxy;
       }
     }
-    c = cn;
-    t = tn;
-    emit = true;
+  };
+  // Two frames of one clip, neither frame 0: one pass over x and both
+  // transforms, six sums per band.
+  auto reduce2 = [&](const Job& ja, const Job& jb) {
+    double* outa = per_clip + (size_t(ja.c) * size_t(nlag) + size_t(ja.t)) * size_t(bands) * 3;
+    double* outb = per_clip + (size_t(jb.c) * size_t(nlag) + size_t(jb.t)) * size_t(bands) * 3;
+    for (int b = wave; b < bands; b += kFusedThreads / 64) {
+      const int s0 = sl[b], s1 = sl[b + 1];
+      double sa = 0, saa = 0, sxa = 0, sb = 0, sbb = 0, sxb = 0;
+      int j = s0 + lane;
+      for (; j + 192 < s1; j += 256) {
+        float xf[4], af[4], bf[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          xf[m] = xl[j + 64 * m];
+          af[m] = dl[j + 64 * m];
+          bf[m] = dl2[j + 64 * m];
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const double x = xf[m], ya = af[m], yb = bf[m];
+          sa += ya;
+          saa = fma(ya, ya, saa);
+          sxa = fma(x, ya, sxa);
+          sb += yb;
+          sbb = fma(yb, yb, sbb);
+          sxb = fma(x, yb, sxb);
+        }
+      }
+      for (; j < s1; j += 64) {
+        const double x = xl[j], ya = dl[j], yb = dl2[j];
+        sa += ya;
+        saa = fma(ya, ya, saa);
+        sxa = fma(x, ya, sxa);
+        sb += yb;
+        sbb = fma(yb, yb, sbb);
+        sxb = fma(x, yb, sxb);
+      }
+      sa = wave_total(sa);
+      saa = wave_total(saa);
+      sxa = wave_total(sxa);
+      sb = wave_total(sb);
+      sbb = wave_total(sbb);
+      sxb = wave_total(sxb);
+      if (lane == 0) {
+        outa[3 * b] = sa;
+        outa[3 * b + 1] = saa;
+        outa[3 * b + 2] = sxa;
+        outb[3 * b] = sb;
+        outb[3 * b + 1] = sbb;
+        outb[3 * b + 2] = sxb;
+      }
+    }
+  };
+
+  Job ja{c_first, 0, t_first == 0};
+  load_z(ja.c, ja.t);
+  __syncthreads();  // every lane has read its positions from inv
+  store_z();
+  __syncthreads();
+  for (int64_t k = 0; k < njobs; k += 2) {
+    const bool has_b = k + 1 < njobs, has_n = k + 2 < njobs;
+    const Job jb = next_job(ja);
+    const Job jn = next_job(jb);
+    if (has_b) load_z(jb.c, jb.t);
+    f32x4 da[HT], db[HT];
+    products(da);     // zl holds frame a
+    __syncthreads();  // every read of zl, and the previous pair's band sums, are done
+    if (has_b) store_z();
+    __syncthreads();
+    if (has_n) load_z(jn.c, jn.t);
+    if (has_b) products(db);  // zl holds frame b
+    __syncthreads();
+    scatter(dl, da);
+    if (has_b) scatter(dl2, db);
+    if (has_n) store_z();
+    __syncthreads();
+    if (has_b && ja.t != 0 && jb.t != 0 && ja.c == jb.c) {
+      reduce2(ja, jb);
+    } else {
+      reduce1(ja, dl);
+      if (has_b) reduce1(jb, dl2);
+    }
+    ja = jn;
   }
 }
 
