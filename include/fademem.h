@@ -17,7 +17,7 @@
  *   Element type is fp32 or bf16 as configured (dtype); LSE is fp32.
  * - Device pointers must be 16-byte aligned; the pool 256-byte aligned.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
- *   Every call except fademem_get_state, fademem_entry_kv,
+ *   Every call except fademem_get_state, fademem_entry_kv, fademem_set_state,
  *   fademem_merge_log and fademem_merge_counts is asynchronous on that stream and never waits for
  *   the device.  One cache is used by one host thread and one stream at a
  *   time.
@@ -200,6 +200,24 @@ int fademem_get_state(fademem_cache* cache, int64_t* count, int64_t* first, int6
  * until the next insert/consolidate.  Synchronises `stream`. */
 int fademem_entry_kv(fademem_cache* cache, int32_t layer, int64_t i, const void** k,
                      const void** v, void* stream);
+
+/* Checkpoint / resume: put a saved memory into a cache that holds nothing
+ * yet (just created, same configuration), so that it continues exactly as
+ * the cache the state was saved from.  count (0..M) entries, oldest first:
+ * first[i], span[i], pos_sum[i] as fademem_get_state returns them, and the
+ * newest inserted position; k[l*count + i], v[l*count + i] (host arrays of
+ * layers*count device pointers, [N][H][D] each) are entry i's K, V of layer
+ * l, e.g. from fademem_entry_kv of the saved cache or the caller's copies of
+ * them (the saved state holds nothing else: entry 0 is the anchor when the
+ * option is on).  The merge log and counts start again from zero.  Copies
+ * on `stream` and synchronises it.  Errors: EINVAL (NULL/misaligned
+ * pointers, count > M, spans < 1, first not increasing by at least the
+ * previous span, pos_sum outside [first*span, newest*span], newest below
+ * the last covered position, positions out of range), ESTATE (the cache
+ * already holds or has held entries), EHIP. */
+int fademem_set_state(fademem_cache* cache, int64_t count, const int64_t* first, const int64_t* span,
+                      const int64_t* pos_sum, int64_t newest, const void* const* k, const void* const* v,
+                      void* stream);
 
 /* Selected pair indices j of the consolidations run so far, oldest first.
  * *total receives how many have run; the most recent min(total, cap, 4096)

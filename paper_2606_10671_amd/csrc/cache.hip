@@ -1093,6 +1093,62 @@ int fademem_entry_kv(fademem_cache* c, int32_t layer, int64_t i, const void** k,
   return FADEMEM_OK;
 }
 
+int fademem_set_state(fademem_cache* c, int64_t count, const int64_t* first, const int64_t* span,
+                      const int64_t* pos_sum, int64_t newest, const void* const* k, const void* const* v,
+                      void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (c->count != 0 || c->any_inserted) return FADEMEM_ESTATE;
+  if (count < 0 || count > c->cfg.budget) return FADEMEM_EINVAL;
+  if (count == 0) return FADEMEM_OK;
+  if (!first || !span || !pos_sum || !k || !v) return FADEMEM_EINVAL;
+  if (newest <= -kMaxPosition || newest >= kMaxPosition) return FADEMEM_EINVAL;
+  int64_t blocks = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    if (first[i] <= -kMaxPosition || first[i] >= kMaxPosition || span[i] < 1 || span[i] > kMaxPosition)
+      return FADEMEM_EINVAL;
+    // the positions an entry covers are distinct integers after the previous entry's and up to newest
+    if (i > 0 && first[i] - first[i - 1] < span[i - 1]) return FADEMEM_EINVAL;
+    const __int128 lo = (__int128)first[i] * span[i], hi = (__int128)newest * span[i];
+    if ((__int128)pos_sum[i] < lo || (__int128)pos_sum[i] > hi) return FADEMEM_EINVAL;
+    blocks += span[i];
+  }
+  if (newest < first[count - 1] + span[count - 1] - 1) return FADEMEM_EINVAL;
+  {
+    const unsigned __int128 mag = (unsigned __int128)(newest < 0 ? -newest : newest) + 1;
+    if (mag * (unsigned __int128)(blocks + 1) >= ((unsigned __int128)1 << 62)) return FADEMEM_EINVAL;
+  }
+  const int layers = c->cfg.layers;
+  for (int64_t q = 0; q < int64_t(layers) * count; ++q)
+    if (!k[q] || !v[q] || !aligned(k[q], 16) || !aligned(v[q], 16)) return FADEMEM_EINVAL;
+  // Entry i goes to slot i (the slot table of a new cache is the identity),
+  // metadata into copy 0.
+  hipStream_t s = as_stream(stream);
+  (void)hipGetLastError();
+  hipError_t e = hipStreamSynchronize(s);  // the cache's initialisation has run
+  if (e != hipSuccess) return hip_fail(c, e);
+  const size_t n = size_t(count) * sizeof(int64_t);
+  if ((e = hipMemcpy(c->pool + c->lay.off_first[0], first, n, hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(c->pool + c->lay.off_span[0], span, n, hipMemcpyHostToDevice)) != hipSuccess ||
+      (e = hipMemcpy(c->pool + c->lay.off_pos_sum[0], pos_sum, n, hipMemcpyHostToDevice)) != hipSuccess)
+    return hip_fail(c, e);
+  for (int l = 0; l < layers; ++l)
+    for (int64_t i = 0; i < count; ++i) {
+      const size_t q = size_t(l) * size_t(count) + size_t(i);
+      if ((e = hipMemcpyAsync(c->pool + kv_offset(c->lay, l, i, 0), k[q], c->lay.blk_bytes, hipMemcpyDeviceToDevice,
+                              s)) != hipSuccess ||
+          (e = hipMemcpyAsync(c->pool + kv_offset(c->lay, l, i, 1), v[q], c->lay.blk_bytes, hipMemcpyDeviceToDevice,
+                              s)) != hipSuccess)
+        return hip_fail(c, e);
+    }
+  if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(c, e);
+  c->cur = 0;
+  c->count = count;
+  c->newest = newest;
+  c->inserted = blocks;
+  c->any_inserted = true;
+  return FADEMEM_OK;
+}
+
 int fademem_merge_log(fademem_cache* c, int32_t* j, int64_t cap, int64_t* total, void* stream) {
   if (!c || !total || cap < 0 || (cap > 0 && !j)) return FADEMEM_EINVAL;
   hipError_t e = hipStreamSynchronize(as_stream(stream));

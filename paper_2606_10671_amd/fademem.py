@@ -32,7 +32,7 @@ MERGE_OPS = {"sqrt_span": FADEMEM_MERGE_SQRT_SPAN, "average": FADEMEM_MERGE_AVER
 EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
     "fademem_consolidate", "fademem_update", "fademem_attend", "fademem_count", "fademem_get_state",
-    "fademem_entry_kv", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
+    "fademem_entry_kv", "fademem_set_state", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
     "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr",
 )
 
@@ -101,6 +101,8 @@ def lib() -> ctypes.CDLL:
     L.fademem_get_state.argtypes = [c_void_p, P(c_int64), P(c_int64), P(c_int64), P(c_int64), P(c_int64),
                                     c_void_p]
     L.fademem_entry_kv.argtypes = [c_void_p, c_int32, c_int64, P(c_void_p), P(c_void_p), c_void_p]
+    L.fademem_set_state.argtypes = [c_void_p, c_int64, P(c_int64), P(c_int64), P(c_int64), c_int64, P(c_void_p),
+                                    P(c_void_p), c_void_p]
     L.fademem_merge_log.argtypes = [c_void_p, P(c_int32), c_int64, P(c_int64), c_void_p]
     L.fademem_merge_counts.argtypes = [c_void_p, P(c_int64), P(c_int64), c_void_p]
     L.fademem_spectral_workspace_bytes.argtypes = [c_int64, c_int64, c_int32, c_int32, c_int32, c_int64,
@@ -200,6 +202,15 @@ def fademem_entry_kv(handle: int, layer: int, i: int, stream: int = 0):
     _ok(lib().fademem_entry_kv(ctypes.c_void_p(handle), layer, i, ctypes.byref(k), ctypes.byref(v),
                                ctypes.c_void_p(stream)), "fademem_entry_kv")
     return k.value, v.value
+
+
+def fademem_set_state(handle: int, count: int, first: Sequence[int], span: Sequence[int], pos_sum: Sequence[int],
+                      newest: int, k_ptrs: Sequence[int], v_ptrs: Sequence[int], stream: int = 0) -> None:
+    n = max(count, 1)
+    arr = lambda xs: (ctypes.c_int64 * n)(*xs)
+    ptrs = lambda xs: (ctypes.c_void_p * max(len(xs), 1))(*xs)
+    _ok(lib().fademem_set_state(ctypes.c_void_p(handle), count, arr(first), arr(span), arr(pos_sum), newest,
+                                ptrs(k_ptrs), ptrs(v_ptrs), ctypes.c_void_p(stream)), "fademem_set_state")
 
 
 def fademem_merge_log(handle: int, cap: int = 4096, stream: int = 0):
@@ -354,6 +365,25 @@ class Cache:
         k = self.pool[kp - base: kp - base + n * elt].view(self.torch_dtype).view(shape)
         v = self.pool[vp - base: vp - base + n * elt].view(self.torch_dtype).view(shape)
         return k, v
+
+    def snapshot(self, stream=None) -> dict:
+        """Checkpoint: the metadata and device copies of every entry's K and V
+        (per layer, oldest first)."""
+        st = self.state(stream)
+        kv = [[tuple(t.clone() for t in self.entry_kv(l, i, stream)) for i in range(st["count"])]
+              for l in range(self.cfg.layers)]
+        return {**st, "kv": kv}
+
+    def restore(self, snap: dict, stream=None):
+        """Resume: put a snapshot of a cache with the same configuration into
+        this one, which must hold nothing yet."""
+        n = snap["count"]
+        ks = [snap["kv"][l][i][0] for l in range(self.cfg.layers) for i in range(n)]
+        vs = [snap["kv"][l][i][1] for l in range(self.cfg.layers) for i in range(n)]
+        for t in ks + vs:
+            self._check(t, self.cfg.tokens_per_block, "entry")
+        fademem_set_state(self.handle, n, snap["first"], snap["span"], snap["pos_sum"], snap["newest"],
+                          [t.data_ptr() for t in ks], [t.data_ptr() for t in vs], self._stream(stream))
 
     def close(self):
         if getattr(self, "handle", None):
