@@ -31,6 +31,11 @@
  *   validation leaves the cache unchanged.  FADEMEM_EHIP reports a HIP
  *   launch or runtime failure (see fademem_last_hip_error).  No C++
  *   exception crosses this interface.
+ * - Debugging: with the environment variable FADEMEM_SERIALIZE set (not
+ *   "0") when a cache is created, every asynchronous call on it waits for
+ *   its own work before returning and reports a failure of that work as
+ *   FADEMEM_EHIP, so an error shows at the call that caused it.  Results
+ *   are the same bits as without it.
  */
 #ifndef FADEMEM_H
 #define FADEMEM_H

@@ -5,6 +5,7 @@
 // Sec. 3.3 (insertion, distance-aware scheduling, consolidation operator,
 // boundary handling) and Algorithm S1 (the complete update).
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
@@ -23,6 +24,7 @@ struct fademem_cache {
   int64_t inserted;     // blocks inserted so far
   int cur;              // metadata copy holding the current state (0 or 1)
   bool any_inserted;
+  bool serialize;       // FADEMEM_SERIALIZE set at creation: every call waits for its work and checks it
   int last_hip_error;
 };
 
@@ -31,6 +33,19 @@ namespace {
 inline size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// End of an asynchronous call: in serialize mode (a debugging aid), wait for
+// the call's work and report a failure at the call that caused it.
+int finish(fademem_cache* c, void* stream) {
+  if (!c->serialize) return FADEMEM_OK;
+  hipError_t e = hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream));
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e != hipSuccess) {
+    c->last_hip_error = int(e);
+    return FADEMEM_EHIP;
+  }
+  return FADEMEM_OK;
+}
 
 int hip_fail(fademem_cache* c, hipError_t e) {
   if (c) c->last_hip_error = int(e);
@@ -824,6 +839,8 @@ int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_
   c->inserted = 0;
   c->cur = 0;
   c->any_inserted = false;
+  const char* ser = getenv("FADEMEM_SERIALIZE");
+  c->serialize = ser && ser[0] && strcmp(ser, "0") != 0;
   c->last_hip_error = 0;
   (void)hipGetLastError();
   const unsigned blocks = unsigned((L.slots + 255) / 256);
@@ -891,7 +908,7 @@ int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v,
   c->inserted += 1;
   c->newest = position;
   c->any_inserted = true;
-  return FADEMEM_OK;
+  return finish(c, stream);
 }
 
 int fademem_consolidate(fademem_cache* c, void* stream) {
@@ -922,7 +939,7 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   if (e != hipSuccess) return hip_fail(c, e);
   c->cur ^= 1;
   c->count -= 1;
-  return FADEMEM_OK;
+  return finish(c, stream);
 }
 
 int fademem_update(fademem_cache* c, const void* const* k, const void* const* v, int64_t frames,
@@ -995,7 +1012,7 @@ int fademem_update(fademem_cache* c, const void* const* k, const void* const* v,
     c->newest = first_position + f0 + nf - 1;
     c->any_inserted = true;
   }
-  return FADEMEM_OK;
+  return finish(c, stream);
 }
 
 int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, const void* k_cur,
@@ -1057,7 +1074,7 @@ int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tok
   hipError_t e = (c->cfg.dtype == FADEMEM_BF16) ? launch_attend_bf16(a, as_stream(stream))
                                                 : launch_attend_f32(a, as_stream(stream));
   if (e != hipSuccess) return hip_fail(c, e);
-  return FADEMEM_OK;
+  return finish(c, stream);
 }
 
 int fademem_get_state(fademem_cache* c, int64_t* count, int64_t* first, int64_t* span, int64_t* pos_sum,
