@@ -47,7 +47,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 # split tiles) at the wan1.3b-1layer workload, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE (see profiles/attend_bf16_wan1.3b_1layer.md), valid only for the
 # kernel source they were taken on (first 16 hex digits of its sha256).
-ATTN_TRAFFIC = {"source_sha256": "1f336d442f3be6c1", "workload": "wan1.3b-1layer", "bytes_per_call": 760845833}
+ATTN_TRAFFIC = {"source_sha256": "ec7c162d9e33a366", "workload": "wan1.3b-1layer", "bytes_per_call": 760797874}
 
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and

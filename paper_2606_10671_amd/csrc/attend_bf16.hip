@@ -17,11 +17,13 @@
 //   B-operand layout of O^T = V^T P^T.
 // * Software pipeline over key tiles of 64: iteration t runs block A =
 //   [S(t+1) = K(t+1) Q^T] beside the exponentials of S(t)'s second 32 keys,
-//   then block B = [O += V(t) P(t)] beside the row max of S(t+1) and the
-//   exponentials of its first 32 keys.  Each block is cut into fenced steps
-//   of four MFMAs that carry their share of the softmax VALU work, the LDS
-//   reads of the next step and one tile load, so one wave always has MFMAs
-//   and independent VALU work in flight.
+//   then block B = [O += V(t) P(t)] beside the exponentials of S(t+1)'s
+//   first 32 keys.  Each block is cut into fenced steps of two MFMAs that
+//   carry their share of the softmax VALU work and the LDS reads of the next
+//   step, so one wave always has MFMAs and independent VALU work in flight.
+//   Block A's first step also issues all global->LDS loads of tile t+2: the
+//   earliest point at which their ring buffer is free, which gives them the
+//   most time to land before the next barrier.
 // * K/V tiles go from global memory straight into LDS (global_load_lds,
 //   16 bytes per lane), issued two tiles ahead into three-deep rings (each
 //   buffer its own LDS object, so the compiler can tell the reads of one
