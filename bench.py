@@ -82,6 +82,8 @@ def parse():
                    help="timed chunks (default: the workload's chunk count minus the warm-up)")
     p.add_argument("--warmup", type=int, default=8)
     p.add_argument("--workload", default="wan1.3b-1layer", choices=sorted(WORKLOADS) + sorted(SPECTRAL))
+    p.add_argument("--budget", type=int, default=None,
+                   help="memory budget M in entries (default: the workload's; 12 is the paper's default, 15 slots with the current chunk)")
     p.add_argument("--beta", type=float, default=0.3)
     p.add_argument("--no-anchor", action="store_true")
     p.add_argument("--merge-op", default="sqrt_span", choices=["sqrt_span", "average", "select_nearest", "max"],
@@ -234,7 +236,11 @@ def main():
     from paper_2606_10671_amd.fademem import Cache
     from paper_2606_10671_amd.synth import TorchWanStream
 
-    wl = WORKLOADS[args.workload]
+    wl = dict(WORKLOADS[args.workload])
+    if args.budget is not None:
+        if args.budget < 1:
+            raise SystemExit("--budget must be at least 1")
+        wl["budget"] = args.budget
     H, D, N, F, M, L = (wl[k] for k in ("heads", "head_dim", "tokens_per_block", "frames", "budget", "layers"))
     anchor = not args.no_anchor
     tdtype = torch.bfloat16 if wl["dtype"] == "bf16" else torch.float32
@@ -428,7 +434,8 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(attn_tflops / peak, 4),
-            "traffic": attn_traffic(args.workload) if is_bf16 else None,
+            "traffic": (attn_traffic(args.workload) if is_bf16 and M == WORKLOADS[args.workload]["budget"]
+                        else None),
             "traffic_unit": "bytes per call (HBM read + write)",
         },
     }

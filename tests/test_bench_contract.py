@@ -45,3 +45,12 @@ def test_measured_traffic_is_tied_to_its_workload():
     assert bench.attn_traffic("wan14b-1layer") is None
     assert bench.measured_traffic(bench.SPEC_TRAFFIC, "spectral.hip", "wan1.3b-1layer") is None
     assert bench.measured_traffic(bench.ATTN_TRAFFIC, "no_such_file.hip", "wan1.3b-1layer") is None
+
+
+def test_budget_override_rejects_an_empty_memory():
+    """`--budget` replaces the workload's M; a budget below one entry is refused before any GPU work."""
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--budget", "0"], capture_output=True,
+                       text=True, timeout=300, cwd=root)
+    assert r.returncode != 0
+    assert "--budget must be at least 1" in r.stderr
