@@ -9,8 +9,14 @@ here); generation happens before the timed region.
 
 Prints ONE JSON line (see the keys below).  Defaults: the Wan-1.3B-class
 single-layer workload (12 heads x 128, 1560 tokens per latent frame,
-3-frame chunks, budget 21, beta 0.3, anchor on, bf16), 8 warm-up chunks
-(the memory fills after 7) and 112 timed chunks = 120 chunks.
+3-frame chunks, budget 21, beta 0.3, anchor on, bf16).  Before the warm-up,
+ceil(M/F) + 1 fill chunks bring the memory to its steady state (full, with
+merges every frame), so every timed chunk attends over M*N + F*N keys and
+runs F merges whatever --warmup says; then the warm-up chunks and the timed
+chunks (8 + 112 by default).  After the headline chunks, a 30-layer leg
+times the chunk update alone (fused, then zero-copy staged), whose working
+set is far above the 256 MB Infinity Cache: that is the merge's HBM
+roofline figure.
 """
 import argparse
 import json
@@ -50,6 +56,12 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 ATTN_TRAFFIC = {"source_sha256": "ec7c162d9e33a366", "workload": "wan1.3b-1layer", "bytes_per_call": 760797874}
 
 
+# HBM bytes of one fused chunk update's data pass (update_data_kernel) in
+# the 30-layer update leg, from rocprofv3 FETCH_SIZE and WRITE_SIZE scaled
+# by the insert copy (see profiles/update_fused_wan1.3b_30layer.md); valid
+# only for the cache.hip source they were taken on.
+UPD_TRAFFIC = {"source_sha256": None, "workload": "wan1.3b-30layer-update", "bytes_per_call": None}
+
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.
 SPEC_TRAFFIC = {"source_sha256": "9ead68d6867c130d", "workload": "spectral-374clips", "bytes_per_call": 1740288092}
@@ -65,7 +77,7 @@ def measured_traffic(table, source, workload):
             sha = hashlib.sha256(f.read()).hexdigest()[:16]
     except OSError:
         return None
-    if sha != table["source_sha256"] or workload != table["workload"]:
+    if table["source_sha256"] is None or sha != table["source_sha256"] or workload != table["workload"]:
         return None
     return table["bytes_per_call"]
 
@@ -100,20 +112,24 @@ def parse():
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-update-leg", action="store_true", help="skip the 30-layer chunk-update leg")
+    p.add_argument("--update-leg-chunks", type=int, default=16, help="timed chunks of each update-leg mode")
     return p.parse_args()
 
 
-def fused_block_ios(js, count0, F, M, anchor, merge_op):
+def fused_block_ios(js, count0, F, M, anchor, merge_op, staged=False):
     """K (or V) block loads and stores of one fused chunk update, replayed
     from the merge decisions the library logged for it (no schedule
     arithmetic here): an operand is loaded once unless it is the result of
     an earlier merge of the same update; every new or changed entry is
-    stored once, and a frame kept as is is also loaded once."""
+    stored once, and a frame kept as is is also loaded once -- unless the
+    frames are staged in pool slots (zero-copy), where a kept frame stays in
+    its slot and moves no bytes."""
     refs = ["old"] * count0
     loads = 0
     it = iter(js)
     for _ in range(F):
-        refs.append("frame")
+        refs.append("old" if staged else "frame")
         if len(refs) > M:
             j = next(it)
             a, b = refs[j], refs[j + 1]
@@ -222,6 +238,90 @@ def run_spectral(args):
     print(json.dumps(result), flush=True)
 
 
+def update_leg(args, M, anchor, L=30, H=12, D=128, N=1560, F=3):
+    """The chunk update alone at the Wan-1.3B-class shape over L layers in
+    one cache (working set ~6.9 GB, far above the 256 MB Infinity Cache):
+    fill the memory, then time `--update-leg-chunks` fused updates
+    (fademem_update: the caller's chunk is read, kept frames are copied into
+    the pool) and as many zero-copy staged updates (fademem_update_staged:
+    the chunk's frames are first written into the staging slots, as the
+    model's K/V projection would, outside the timed calls).  Events bracket
+    each update call on its stream; bytes are the algorithmic bytes replayed
+    from the logged merge decisions."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    from paper_2606_10671_amd.synth import TorchWanStream
+    dev = torch.device("cuda", 0)
+    T = args.update_leg_chunks
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=args.beta, anchor=anchor,
+                  dtype=torch.bfloat16, layers=L, device=dev, merge_op=args.merge_op, stage_frames=F)
+    distinct = 4
+    streams = [TorchWanStream(args.seed + 7000 + 1000 * l, N, H, D, device=dev) for l in range(L)]
+    data = []
+    for _ in range(distinct):
+        per_layer = []
+        for l in range(L):
+            _, k, v = streams[l].chunk(F)
+            per_layer.append((k.to(torch.bfloat16).contiguous(), v.to(torch.bfloat16).contiguous()))
+        data.append(per_layer)
+    stream = torch.cuda.current_stream()
+    fill = -(-M // F) + 1
+    c = 0
+    for _ in range(fill):
+        d = data[c % distinct]
+        cache.update([x[0] for x in d], [x[1] for x in d], c * F)
+        c += 1
+    torch.cuda.synchronize()
+    blk = N * H * D * 2
+    modes = {}
+    for mode in ("fused", "staged"):
+        evs = []
+        c0 = c
+        for _ in range(T):
+            d = data[c % distinct]
+            if mode == "staged":
+                slots = cache.stage(F)
+                for l in range(L):
+                    for f in range(F):
+                        slots[l][f][0].copy_(d[l][0][f * N:(f + 1) * N])
+                        slots[l][f][1].copy_(d[l][1][f * N:(f + 1) * N])
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if mode == "fused":
+                cache.update([x[0] for x in d], [x[1] for x in d], c * F)
+            else:
+                cache.update_staged(F, c * F)
+            e1.record(stream)
+            evs.append((e0, e1))
+            c += 1
+        torch.cuda.synchronize()
+        ms = [a.elapsed_time(b) for a, b in evs]
+        _, log = cache.merge_log(cap=4096)
+        js = log[len(log) - T * F:]
+        bytes_ = 0
+        for i in range(T):
+            loads, stores = fused_block_ios(js[i * F:(i + 1) * F], M, F, M, anchor, args.merge_op,
+                                            staged=(mode == "staged"))
+            bytes_ += (loads + stores) * 2 * blk * L
+        t_s = sum(ms) / 1e3
+        modes[mode] = {"ms_per_update": round(sum(ms) / len(ms), 4),
+                       "bytes_per_update": int(bytes_ // T),
+                       "gbps": round(bytes_ / t_s / 1e9, 1) if bytes_ else None,
+                       "first_chunk": c0, "chunks": T}
+    cache.verify()
+    del cache, data
+    torch.cuda.empty_cache()
+    fused = modes["fused"]
+    traffic = measured_traffic(UPD_TRAFFIC, "cache.hip", "wan1.3b-30layer-update") if M == 21 else None
+    roof = {"bound": "hbm", "kernel": f"update_plan_kernel + update_data_kernel (one fademem_update call, {L} layers)",
+            "achieved": fused["gbps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(fused["gbps"] / HBM_PEAK_GBS, 4) if fused["gbps"] else None,
+            "traffic": traffic, "traffic_unit": "bytes per call (HBM read + write)",
+            "algorithmic_bytes": fused["bytes_per_update"],
+            "workload": f"wan1.3b-{L}layer-update (12x128 heads, 1560 tokens/frame, 3-frame chunks, budget {M})"}
+    return roof, {"layers": L, **modes}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -238,17 +338,21 @@ def main():
 
     wl = dict(WORKLOADS[args.workload])
     if args.budget is not None:
-        if args.budget < 1:
-            raise SystemExit("--budget must be at least 1")
+        if args.budget < 2:
+            raise SystemExit("--budget must be at least 2 (one eligible pair besides the newest entry)")
         wl["budget"] = args.budget
     H, D, N, F, M, L = (wl[k] for k in ("heads", "head_dim", "tokens_per_block", "frames", "budget", "layers"))
     anchor = not args.no_anchor
     tdtype = torch.bfloat16 if wl["dtype"] == "bf16" else torch.float32
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    # Fill chunks: the memory holds M entries after ceil(M/F) chunks; one
+    # more makes every later chunk's updates merge once per frame.
+    fill = -(-M // F) + 1
     if args.steps is None:
-        args.steps = wl["chunks"] - args.warmup
-    chunks = args.warmup + args.steps
+        args.steps = max(1, wl["chunks"] - args.warmup - fill)
+    chunks = fill + args.warmup + args.steps
+    first_timed = fill + args.warmup
 
     # ---- inputs, resident in HBM before timing -------------------------------
     # Distinct chunks are generated up to ~16 GB and then reused cyclically
@@ -283,6 +387,7 @@ def main():
                 if ev is not None:
                     ev["attn"].append(new_pair())
                     ev["attn"][-1][0].record(stream)
+                    ev["keys"].append(cache.count() * N + F * N)  # host mirror of the count: no sync
                 cache.attend(q, k, v, layer=l, out=out)
                 if ev is not None:
                     ev["attn"][-1][1].record(stream)
@@ -311,7 +416,7 @@ def main():
         if ev is not None:
             ev["upd"][-1][1].record(stream)
 
-    for c in range(args.warmup):
+    for c in range(first_timed):
         chunk_step(c)
     torch.cuda.synchronize()
     merges_before, anchor_before = cache.merge_counts()
@@ -319,12 +424,12 @@ def main():
     # ---- timed region: whole chunk steps, with events around every call on
     # the stream the kernels run on (per-kernel averages come from these) -----
     t_start, t_end = new_pair()
-    ev = {"attn": [], "ins": [], "cons": [], "upd": []}
+    ev = {"attn": [], "keys": [], "ins": [], "cons": [], "upd": []}
     marks = []
     torch.cuda.synchronize()
     t_start.record(stream)
     t_prog = time.time()
-    for c in range(args.warmup, chunks):
+    for c in range(first_timed, chunks):
         marks.append(torch.cuda.Event(enable_timing=True))
         marks[-1].record(stream)
         chunk_step(c, ev)
@@ -348,9 +453,10 @@ def main():
     weighted = (total_merges - merges_before) - (anchor_total - anchor_before)
     blk = frame_elems * elt
     lk = M * N + F * N                      # keys per attention call at steady state
-    attn_flop = 4.0 * (F * N) * lk * D * H  # QK^T and PV, per layer-call
+    assert all(k == lk for k in ev["keys"]), "a timed attention call saw a memory that is not full"
+    attn_flop = sum(4.0 * (F * N) * k * D * H for k in ev["keys"])  # QK^T and PV of every timed call
     attn_avg_s = sum(attn_ms) / len(attn_ms) / 1e3
-    attn_tflops = attn_flop / attn_avg_s / 1e12
+    attn_tflops = attn_flop / (sum(attn_ms) / 1e3) / 1e12
     # A weighted (or averaged, or max-pooled) merge reads two entries' K and V
     # and writes one; Select Nearest re-points a slot and moves no bytes.
     merge_bytes = 0 if args.merge_op == "select_nearest" else weighted * 3 * 2 * blk * L
@@ -372,7 +478,7 @@ def main():
                     m += 1
             per_chunk_merges.append(m)
         _, log = cache_timed.merge_log(cap=4096)
-        timed = list(range(args.warmup, chunks))
+        timed = list(range(first_timed, chunks))
         while timed and sum(per_chunk_merges[c] for c in timed) > len(log):
             timed.pop(0)
         js = log[len(log) - sum(per_chunk_merges[c] for c in timed):]
@@ -382,7 +488,7 @@ def main():
             loads, stores = fused_block_ios(js[pos:pos + n], count0s[c], F, M, anchor, args.merge_op)
             pos += n
             bytes_ += (loads + stores) * 2 * blk * L
-        t_s = sum(upd_ms[c - args.warmup] for c in timed) / 1e3
+        t_s = sum(upd_ms[c - first_timed] for c in timed) / 1e3
         update_gbps = bytes_ / t_s / 1e9 if t_s > 0 and bytes_ > 0 else None
 
     state = cache_timed.state()
@@ -396,6 +502,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "fill_chunks": fill,
         "ms_per_step": round(ms_chunk, 4),
         "ms_per_chunk_median": round(ms_median, 4),
         "higher_is_better": False,
@@ -455,6 +562,18 @@ def main():
                     fill_v.append(host(vc[f * N:(f + 1) * N]))
             return host(q), host(k), host(v), fill_k, fill_v
         result["cpu_baseline"] = cpu_baseline(wl, head_inputs, args.beta, anchor, args.cpu_seconds, args.merge_op)
+    if not args.no_update_leg and args.workload.startswith("wan1.3b") and wl["dtype"] == "bf16":
+        if L == 1:
+            del inputs, cache, cache_timed
+            torch.cuda.empty_cache()
+            inputs = None
+            result["merge_roofline"], result["update_leg"] = update_leg(args, M, anchor)
+        elif update_gbps:
+            result["merge_roofline"] = {
+                "bound": "hbm", "kernel": f"update_plan_kernel + update_data_kernel (one fademem_update call, {L} layers)",
+                "achieved": round(update_gbps, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(update_gbps / HBM_PEAK_GBS, 4), "traffic": None,
+                "traffic_unit": "bytes per call (HBM read + write)", "workload": args.workload}
     print(json.dumps(result), flush=True)
 
 

@@ -18,9 +18,14 @@
  * - Device pointers must be 16-byte aligned; the pool 256-byte aligned.
  * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *   Every call except fademem_get_state, fademem_entry_kv, fademem_set_state,
- *   fademem_merge_log and fademem_merge_counts is asynchronous on that stream and never waits for
- *   the device.  One cache is used by one host thread and one stream at a
- *   time.
+ *   fademem_merge_log, fademem_merge_counts and fademem_verify is
+ *   asynchronous on that stream and never waits for the device
+ *   (fademem_stage and fademem_count only read host state).  One cache is
+ *   used by one host thread and one stream at a time.
+ * - Calls that implement a step of the method cite the passage that defines
+ *   it; the plumbing around them (pool sizing, creation, readers,
+ *   checkpointing, error strings) has no counterpart in the paper and cites
+ *   none.
  * - Ownership: the caller allocates and owns the device pool and every
  *   Q/K/V/O/LSE buffer.  The library allocates no device memory, never
  *   frees caller memory and keeps only the pool pointer.  insert copies K
@@ -53,7 +58,9 @@ enum {
   FADEMEM_ESTATE = -2,     /* call not allowed in the current memory state       */
   FADEMEM_ENOMEM = -3,     /* caller's pool smaller than fademem_pool_bytes      */
   FADEMEM_EHIP = -4,       /* HIP runtime or launch error                        */
-  FADEMEM_EUNSUPPORTED = -5/* valid request this build does not implement        */
+  FADEMEM_EUNSUPPORTED = -5,/* valid request this build does not implement       */
+  FADEMEM_EINTERNAL = -6   /* host replay of the memory state disagrees with the
+                              device (fademem_verify, serialize mode)           */
 };
 
 enum { FADEMEM_F32 = 0, FADEMEM_BF16 = 1 };
@@ -109,16 +116,20 @@ typedef struct fademem_config {
                                chunk's queries and keys at indices n + f (n =
                                entries held, f = frame within the chunk).    */
   double  rope_theta;       /* rotary base (> 1), e.g. 10000; ignored if P = 0 */
+  int32_t stage_frames;     /* 0..4: frames a chunk may stage for the
+                               zero-copy update (fademem_stage); 0 = off.
+                               The pool then holds M + max(1, stage_frames)
+                               KV slots per layer.                            */
 } fademem_config;
 
 typedef struct fademem_cache fademem_cache; /* opaque host object */
 
-/* Bytes of device pool a configuration needs: (M+1) KV slots per layer for
- * K and V, the memory's metadata, the attention's scratch for split work
- * (bf16: partial results of split query tiles, 69.2 MB at D = 128; fp32:
- * partial results of key ranges, 512 x 64 x (D+2) floats) and, with
- * rope_pairs > 0, the re-indexed view of M entries' K and V.  Returns
- * EINVAL for a bad config. */
+/* Bytes of device pool a configuration needs: M + max(1, stage_frames) KV
+ * slots per layer for K and V, the memory's metadata, the attention's
+ * scratch for split work (bf16: partial results of split query tiles,
+ * 70.3 MB at D = 128; fp32: partial results of key ranges, 512 x 64 x (D+2)
+ * floats) and, with rope_pairs > 0, a re-indexed K view per layer (one K
+ * block per slot).  Returns EINVAL for a bad config. */
 int fademem_pool_bytes(const fademem_config* cfg, size_t* bytes);
 
 /* Create a cache over a caller-owned device pool of `pool_bytes` bytes
@@ -176,6 +187,33 @@ int fademem_consolidate(fademem_cache* cache, void* stream);
  * entries held), EHIP. */
 int fademem_update(fademem_cache* cache, const void* const* k, const void* const* v, int64_t frames,
                    int64_t first_position, void* stream);
+
+/* Zero-copy insert (Alg. S1 "Append"; Sec. 4.1 and supplementary Sec. S4:
+ * one entry per latent frame, the memory updated once the chunk is
+ * generated).  With stage_frames > 0, the caller's projection can write a
+ * chunk's K/V straight into free pool slots instead of its own buffers:
+ * fademem_stage returns, for frame f < frames of layer l, the device
+ * address of the K block k[l*frames + f] and of the V block
+ * v[l*frames + f] ([N][H][D] each; the frames of a chunk are separate
+ * blocks).  It reads host state only and enqueues nothing; the addresses
+ * stay valid until the next insert, consolidate or update.
+ * fademem_update_staged(frames, first_position) then runs the same F
+ * Alg. S1 updates as fademem_update with frame f taken from its staging
+ * slot: a frame that survives stays where the caller wrote it (no copy) and
+ * one that a merge consumes frees its slot.  State, merge log and stored
+ * K/V bits equal those of fademem_update on the same frames.
+ * fademem_attend_staged attends over [memory || staged frames] (the
+ * generator's final pass over a chunk, whose K/V become the update's).
+ * The free slots are known on the host because the library replays every
+ * update's schedule on the host copy of the integer metadata (the device
+ * still makes the decisions; fademem_verify checks that both agree).
+ * Limits: 1 <= frames <= stage_frames <= 4.  Errors: EINVAL (frames out of
+ * range, NULL pointers, positions out of range), ESTATE (M+1 entries held,
+ * position not above the newest), EHIP. */
+int fademem_stage(fademem_cache* cache, int64_t frames, void** k, void** v);
+int fademem_update_staged(fademem_cache* cache, int64_t frames, int64_t first_position, void* stream);
+int fademem_attend_staged(fademem_cache* cache, int32_t layer, const void* q, int64_t q_tokens,
+                          int64_t frames, float scale, void* out, float* lse, void* stream);
 
 /* Attention of the chunk's queries over layer `layer`'s exposed cache:
  * O_h = softmax(scale * Q_h K_h^T) V_h per head, with the keys/values
@@ -261,6 +299,12 @@ int fademem_spectral_workspace_bytes(int64_t clips, int64_t frames, int32_t heig
 int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, int32_t height,
                           int32_t width, const int32_t* band_of, int32_t bands, int64_t max_lag,
                           void* workspace, size_t workspace_bytes, double* corr, void* stream);
+
+/* Synchronise `stream` and compare the host replay of the memory (spans,
+ * positions, slot table) with the device's state.  Returns OK or
+ * EINTERNAL (serialize mode runs the same check after every call).
+ * Errors: EINVAL (NULL cache), EHIP. */
+int fademem_verify(fademem_cache* cache, void* stream);
 
 /* hipError_t value of the last FADEMEM_EHIP on this cache (0 if none). */
 int fademem_last_hip_error(const fademem_cache* cache);

@@ -39,8 +39,10 @@
 //   last key again and score -inf.
 // * Online softmax in base 2 with the scale folded into one FMA; O is
 //   rescaled only when a row max grows by more than 2^8 (the stale max
-//   cancels in the final normalisation).  The denominator sums the
-//   bf16-rounded weights that enter the P.V product.
+//   cancels in the final normalisation).  O's denominator sums the
+//   bf16-rounded weights that enter the P.V product; when the caller asks
+//   for the log-sum-exp, a second fp32 sum of the unrounded weights gives
+//   it (the kernel variant without LSE output skips that sum).
 // * Workgroup index -> work is remapped so that one XCD runs a contiguous
 //   range of (head, query tile) and shares K/V in its L2.
 #include <mutex>
@@ -161,7 +163,7 @@ __device__ __forceinline__ int xcd_group(int bid, int groups) {
 // LSE.
 template <int D>
 __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (&o)[Shape<D>::DB], float m_scaled,
-                                          float l_tot, int q_row, int h, int hh) {
+                                          float l_tot, float l_lse, int q_row, int h, int hh) {
   const int H = args.heads;
   const int Lq = int(args.q_tokens);
   if (q_row >= Lq) return;
@@ -177,17 +179,17 @@ __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (
       const int d = 32 * db + 8 * g4 + 4 * hh;
       *reinterpret_cast<bf16x4*>(obase + d * 2) = v;
     }
-  if (args.lse && hh == 0) args.lse[size_t(h) * Lq + q_row] = (m_scaled + __log2f(l_tot)) * kLn2;
+  if (args.lse && hh == 0) args.lse[size_t(h) * Lq + q_row] = (m_scaled + __log2f(l_lse)) * kLn2;
 }
 
 // Scratch slot layout of a partial result: O registers lane-major,
-// [wave][qb][db][r][lane], then m and l per (qb, thread).
+// [wave][qb][db][r][lane], then m, l and the unrounded sum per (qb, thread).
 template <int D>
 __device__ __forceinline__ size_t ws_o_index(int wave, int qb, int db, int r, int lane) {
   return ((size_t((wave * QB + qb) * Shape<D>::DB + db) * 16 + r) * 64 + lane);
 }
 
-template <int D, bool WIDE>
+template <int D, bool WIDE, bool LSE>
 __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const SkPlan& plan) {
   using S = Shape<D>;
   // Three-deep rings of K and V tile buffers, each a separate LDS object.
@@ -197,11 +199,12 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
   __shared__ __attribute__((aligned(16))) char v_lds0[S::TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char v_lds1[S::TILE_BYTES];
   __shared__ __attribute__((aligned(16))) char v_lds2[S::TILE_BYTES];
-  // Entry table: K address of row 0 (head 0) of each memory entry, and the
-  // current chunk as entry n_entries; V is v_offset (memory) or v_cur-k_cur
-  // (current chunk) bytes further.
+  // Entry table: K address of row 0 (head 0) of each exposed entry, and the
+  // current chunk as entry n_entries; its V rows are ent_vd[e] bytes from
+  // its K rows.
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const char** ent_k = reinterpret_cast<const char**>(smem);
+  long long* ent_vd = reinterpret_cast<long long*>(smem + (size_t(args.n_entries) + 1) * sizeof(const char*));
 
   const int g = xcd_group(blockIdx.x, gridDim.x);
   const int tid = threadIdx.x;
@@ -218,12 +221,18 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
   const int Lq = int(args.q_tokens);
   const size_t row_bytes = size_t(H) * D * 2;
   const char* k_cur = static_cast<const char*>(args.k_cur);
-  const long long mem_vdelta = (long long)args.v_offset;
-  const long long cur_vdelta = static_cast<const char*>(args.v_cur) - k_cur;
   const int mem_rows = n_entries * N;
 
-  for (int e = tid; e < n_entries + 1; e += kThreads)
-    ent_k[e] = (e < n_entries) ? args.kv_layer_base + size_t(args.order[e]) * args.slot_stride : k_cur;
+  for (int e = tid; e < n_entries + 1; e += kThreads) {
+    const char* kp = k_cur;
+    const char* vp = static_cast<const char*>(args.v_cur);
+    if (e < n_entries) {
+      kp = args.k_base + size_t(args.k_order ? args.k_order[e] : e) * args.k_stride;
+      vp = args.v_base + size_t(args.v_order[e]) * args.v_stride;
+    }
+    ent_k[e] = kp;
+    ent_vd[e] = vp - kp;
+  }
 
   // Per-lane constants of the tile loads: load i writes destination chunk
   // q = (i*waves + wave)*64 + lane = row n0, LDS position p; it fetches global
@@ -292,10 +301,10 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     long long last_vd;
     if (cur_tokens > 0) {
       last_k = k_cur + size_t(cur_tokens - 1) * row_bytes + head_off;
-      last_vd = cur_vdelta;
+      last_vd = ent_vd[n_entries];
     } else {
       last_k = ent_k[n_entries - 1] + size_t(N - 1) * row_bytes + head_off;
-      last_vd = mem_vdelta;
+      last_vd = ent_vd[n_entries - 1];
     }
 
     // Load stream: the next tile to load starts in entry ld_e at row ld_off
@@ -330,8 +339,8 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         tr.ncross = in_mem0 ? N - ld_off : kBN;
         tr.base0 = ent_k[ld_e] + head_off + (long long)ld_off * (long long)row_bytes;
         tr.base1 = ent_k[e1] + head_off - (long long)tr.ncross * (long long)row_bytes;
-        tr.vd0 = in_mem0 ? mem_vdelta : cur_vdelta;
-        tr.vd1 = e1 < n_entries ? mem_vdelta : cur_vdelta;
+        tr.vd0 = ent_vd[ld_e];
+        tr.vd1 = ent_vd[e1];
         ld_off += kBN;
         if (in_mem0 && ld_off >= N) {
           ld_off -= N;
@@ -359,10 +368,10 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         } else if (k < mem_rows) {
           const int e = k / N;
           row = ent_k[e] + head_off + size_t(k - e * N) * row_bytes;
-          vd = mem_vdelta;
+          vd = ent_vd[e];
         } else {
           row = k_cur + head_off + size_t(k - mem_rows) * row_bytes;
-          vd = cur_vdelta;
+          vd = ent_vd[n_entries];
         }
       }
       const int j = i * kWaves + wave;
@@ -398,17 +407,19 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
       for (int db = 0; db < S::DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[qb][db][r] = 0.0f;
-    float m_run[QB], l_run[QB];
+    float m_run[QB], l_run[QB], lu_run[QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       m_run[qb] = -INFINITY;  // running (possibly stale) max of raw scores
-      l_run[qb] = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2)
+      l_run[qb] = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2), rounded to bf16
+      lu_run[qb] = 0.0f;      // the same sum of the unrounded weights (LSE only)
     }
 
     const int partial_tile = (Lk % kBN) ? (Lk / kBN) : -1;  // the tile with keys >= Lk, if any
     f32x16 s_cur[2][QB];  // S^T of the current tile [nb][qb]
     u32x4 p_cur[4][QB];   // P of the current tile [ks][qb] (bf16 pairs)
     float ps_cur[QB];     // this lane's sum of the current tile's P so far
+    float pu_cur[QB];     // the same of the unrounded weights (LSE only)
 
     // Softmax without a per-tile row max: a tile's weights are taken against
     // the running max m_run as it stands.  If any weight of a row exceeds
@@ -422,11 +433,12 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     // in block B, the rest in the next block A.
     constexpr int kPairs = 16 * QB;
     constexpr int kPairsB = 8 * QB;
-    auto exp_pair = [&](const f32x16 (&s)[2][QB], u32x4 (&p)[4][QB], float (&ps)[QB], int pi) {
+    auto exp_pair = [&](const f32x16 (&s)[2][QB], u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB], int pi) {
       const int qb = pi / 16, rr = pi % 16, nb = rr / 8, r = 2 * (rr % 8);
       const float mc = m_run[qb] * c2;
       const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r], c2, -mc));
       const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r + 1], c2, -mc));
+      if constexpr (LSE) pu[qb] = (pu[qb] + p0) + p1;
       const uint32_t w = round_and_sum(p0, p1, ps[qb]);
       asm volatile("" ::"v"(w));  // keep the weight in its pipeline step
       p[2 * nb + (r >> 3)][qb][(r & 7) >> 1] = w;
@@ -482,7 +494,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     // Redo a tile against the exact running max: its scores again from its K
     // buffer, new m_run, rescale O and l, recompute all its weights and the
     // tile sum.
-    auto redo_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
+    auto redo_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB]) {
       f32x16 s[2][QB];
       qk_tile(tile, kb_lds, s);
       float mx[QB];
@@ -493,24 +505,29 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         const float alpha = __builtin_amdgcn_exp2f((m_run[qb] - m_new) * c2);
         m_run[qb] = m_new;
         l_run[qb] *= alpha;
+        if constexpr (LSE) lu_run[qb] *= alpha;
 #pragma unroll
         for (int db = 0; db < S::DB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[qb][db][r] *= alpha;
         ps[qb] = 0.0f;
+        pu[qb] = 0.0f;
       }
 #pragma unroll
-      for (int pi = 0; pi < kPairs; ++pi) exp_pair(s, p, ps, pi);
+      for (int pi = 0; pi < kPairs; ++pi) exp_pair(s, p, ps, pu, pi);
     };
     // End of a tile's weights: redo it if a weight grew past 2^8, then add
     // its sum to l.
-    auto close_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
+    auto close_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB]) {
       bool grow = false;
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) grow = grow || !(ps[qb] <= kRescaleBound);
-      if (__any(grow)) redo_tile(tile, kb_lds, p, ps);
+      if (__any(grow)) redo_tile(tile, kb_lds, p, ps, pu);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) l_run[qb] += ps[qb];
+      for (int qb = 0; qb < QB; ++qb) {
+        l_run[qb] += ps[qb];
+        if constexpr (LSE) lu_run[qb] += pu[qb];
+      }
     };
     auto read_k = [&](const char* kb_lds, int kb, bf16x8 (&kf)[2]) {
       kf[0] = *reinterpret_cast<const bf16x8*>(kb_lds + k_rd[kb]);
@@ -591,10 +608,10 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         }
 #pragma unroll
         for (int pi = kPairsB; pi < kPairs; ++pi)
-          if (st == (pi - kPairsB) * S::KB / (kPairs - kPairsB)) exp_pair(s_cur, p_cur, ps_cur, pi);
+          if (st == (pi - kPairsB) * S::KB / (kPairs - kPairsB)) exp_pair(s_cur, p_cur, ps_cur, pu_cur, pi);
         __builtin_amdgcn_sched_barrier(0);
       }
-      close_tile(t, kbuf[b], p_cur, ps_cur);  // tile t's K buffer is refilled only in the next block A
+      close_tile(t, kbuf[b], p_cur, ps_cur, pu_cur);  // tile t's K buffer is refilled only in the next block A
       __builtin_amdgcn_sched_barrier(0);
 
       // Block B: O += V(t) P(t), two 32-row blocks of one k-step per step,
@@ -603,9 +620,12 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         if (maskn) mask(t + 1, s_next);
       }
       u32x4 p_next[4][QB];
-      float ps_next[QB];
+      float ps_next[QB], pu_next[QB];
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) ps_next[qb] = 0.0f;
+      for (int qb = 0; qb < QB; ++qb) {
+        ps_next[qb] = 0.0f;
+        pu_next[qb] = 0.0f;
+      }
 #pragma unroll
       for (int st = 0; st < kStepsB; ++st) {
         const int ks = st / (S::DB / kDbPerStep), db0 = (st % (S::DB / kDbPerStep)) * kDbPerStep;
@@ -625,7 +645,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         if constexpr (NEXT) {
 #pragma unroll
           for (int pi = 0; pi < kPairsB; ++pi)
-            if (st == pi * kStepsB / kPairsB) exp_pair(s_next, p_next, ps_next, pi);
+            if (st == pi * kStepsB / kPairsB) exp_pair(s_next, p_next, ps_next, pu_next, pi);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -639,6 +659,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
 #pragma unroll
           for (int ks = 0; ks < 4; ++ks) p_cur[ks][qb] = p_next[ks][qb];
           ps_cur[qb] = ps_next[qb];
+          pu_cur[qb] = pu_next[qb];
         }
       }
     };
@@ -654,9 +675,12 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
       qk_tile(kt0, kbuf[0], s_cur);
       row_max(s_cur, m_run);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) ps_cur[qb] = 0.0f;
+      for (int qb = 0; qb < QB; ++qb) {
+        ps_cur[qb] = 0.0f;
+        pu_cur[qb] = 0.0f;
+      }
 #pragma unroll
-      for (int pi = 0; pi < kPairsB; ++pi) exp_pair(s_cur, p_cur, ps_cur, pi);
+      for (int pi = 0; pi < kPairsB; ++pi) exp_pair(s_cur, p_cur, ps_cur, pu_cur, pi);
     }
 
     using I0 = std::integral_constant<int, 0>;
@@ -695,8 +719,8 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     if (slot < 0) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
-        store_out<D>(args, o[qb], m_run[qb] * c2, pair_sum(l_run[qb]), qt * kBM + wave * kQW + 32 * qb + l32, h,
-                     hh);
+        store_out<D>(args, o[qb], m_run[qb] * c2, pair_sum(l_run[qb]), LSE ? pair_sum(lu_run[qb]) : 1.0f,
+                     qt * kBM + wave * kQW + 32 * qb + l32, h, hh);
     } else {
       float* ws = args.ws + size_t(slot) * attend_slot_floats(D);
 #pragma unroll
@@ -707,6 +731,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
           for (int r = 0; r < 16; ++r) ws[ws_o_index<D>(wave, qb, db, r, lane)] = o[qb][db][r];
         ws[kBM * D + qb * kThreads + tid] = m_run[qb];
         ws[kBM * D + (QB + qb) * kThreads + tid] = l_run[qb];
+        if constexpr (LSE) ws[kBM * D + (2 * QB + qb) * kThreads + tid] = lu_run[qb];
       }
     }
   };
@@ -756,41 +781,57 @@ __device__ __forceinline__ void attend_bf16_merge_body(const AttendArgs& args, c
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int mi = kBM * D + qb * kThreads + tid, li = kBM * D + (QB + qb) * kThreads + tid;
+    const int ui = kBM * D + (2 * QB + qb) * kThreads + tid;
     const float m_max = fmaxf(part[0][mi], part[1][mi]);
     f32x16 o[S::DB];
 #pragma unroll
     for (int db = 0; db < S::DB; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-    float l_tot = 0.0f;
+    float l_tot = 0.0f, l_lse = 0.0f;
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const float* ws = part[p];
       const float f = __builtin_amdgcn_exp2f((ws[mi] - m_max) * c2);
       l_tot += f * pair_sum(ws[li]);
+      if (args.lse) l_lse += f * pair_sum(ws[ui]);
 #pragma unroll
       for (int db = 0; db < S::DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] += f * ws[ws_o_index<D>(wave, qb, db, r, lane)];
     }
-    store_out<D>(args, o, m_max * c2, l_tot, (qg % plan.q_tiles) * kBM + wave * kQW + 32 * qb + l32,
+    store_out<D>(args, o, m_max * c2, l_tot, l_lse, (qg % plan.q_tiles) * kBM + wave * kQW + 32 * qb + l32,
                  qg / plan.q_tiles, hh);
   }
 }
 
 }  // namespace
 
+// Kernels: head dimension, entries of at least one key tile (or shorter),
+// with or without the log-sum-exp output.
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, true>(args, plan);
+  attend_bf16_body<128, true, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, true>(args, plan);
+  attend_bf16_body<64, true, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_short(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, false>(args, plan);
+  attend_bf16_body<128, false, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_short(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, false>(args, plan);
+  attend_bf16_body<64, false, false>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_lse(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<128, true, true>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_lse(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<64, true, true>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_short_lse(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<128, false, true>(args, plan);
+}
+__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_short_lse(AttendArgs args, SkPlan plan) {
+  attend_bf16_body<64, false, true>(args, plan);
 }
 __global__ __launch_bounds__(kThreads) void attend_bf16_merge_d128(AttendArgs args, SkPlan plan) {
   attend_bf16_merge_body<128>(args, plan);
@@ -812,7 +853,7 @@ hipError_t launch_d(AttnKernel kernel, AttnKernel merge, std::once_flag& attr_on
   plan.q_tiles = int(q_tiles64);
   plan.tiles = int((lk + kBN - 1) / kBN);
   const int total = plan.q_tiles * a.heads;
-  const size_t shmem = size_t(a.n_entries + 1) * 8;  // entry table; tile buffers are static
+  const size_t shmem = size_t(a.n_entries + 1) * 16;  // entry table; tile buffers are static
   if (shmem > 32 * 1024) return hipErrorInvalidValue;
   hipError_t e = hipSuccess;
   std::call_once(attr_once, [&] {
@@ -852,18 +893,20 @@ hipError_t launch_d(AttnKernel kernel, AttnKernel merge, std::once_flag& attr_on
   return e;
 }
 
-std::once_flag attr_d128, attr_d64, attr_d128s, attr_d64s;
+std::once_flag attr_once[8];
 
 }  // namespace
 
 hipError_t launch_attend_bf16(const AttendArgs& a, hipStream_t stream) {
   const bool wide = a.tokens_per_block >= kBN;
-  if (a.head_dim == 128)
-    return wide ? launch_d(attend_bf16_d128, attend_bf16_merge_d128, attr_d128, a, stream)
-                : launch_d(attend_bf16_d128_short, attend_bf16_merge_d128, attr_d128s, a, stream);
-  if (a.head_dim == 64)
-    return wide ? launch_d(attend_bf16_d64, attend_bf16_merge_d64, attr_d64, a, stream)
-                : launch_d(attend_bf16_d64_short, attend_bf16_merge_d64, attr_d64s, a, stream);
+  const bool lse = a.lse != nullptr;
+  static const AttnKernel k128[2][2] = {{attend_bf16_d128_short, attend_bf16_d128_short_lse},
+                                        {attend_bf16_d128, attend_bf16_d128_lse}};
+  static const AttnKernel k64[2][2] = {{attend_bf16_d64_short, attend_bf16_d64_short_lse},
+                                       {attend_bf16_d64, attend_bf16_d64_lse}};
+  const int w = wide ? 1 : 0, l = lse ? 1 : 0;
+  if (a.head_dim == 128) return launch_d(k128[w][l], attend_bf16_merge_d128, attr_once[w * 2 + l], a, stream);
+  if (a.head_dim == 64) return launch_d(k64[w][l], attend_bf16_merge_d64, attr_once[4 + w * 2 + l], a, stream);
   return hipErrorInvalidValue;
 }
 

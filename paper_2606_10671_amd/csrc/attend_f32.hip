@@ -54,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void attend_f32_kernel(AttendArgs args, i
   using SM = F32Smem<D>;
   constexpr int HD = SM::HD;
   __shared__ __attribute__((aligned(16))) float smem[SM::floats];
-  extern __shared__ int32_t order_s[];
+  extern __shared__ int32_t order_s[];  // K block index of entry e at 2e, V block index at 2e + 1
 
   const int part = blockIdx.x % parts;
   const int h = (blockIdx.x / parts) / q_tiles;
@@ -76,7 +76,10 @@ __global__ __launch_bounds__(kThreads) void attend_f32_kernel(AttendArgs args, i
   const size_t row_bytes = size_t(H) * D * 4;
   const size_t head_off = size_t(h) * D * 4;
 
-  for (int e = tid; e < n_entries; e += kThreads) order_s[e] = args.order[e];
+  for (int e = tid; e < n_entries; e += kThreads) {
+    order_s[2 * e] = args.k_order ? args.k_order[e] : e;
+    order_s[2 * e + 1] = args.v_order[e];
+  }
 
   const float c2 = args.scale * kLog2e;  // scores in the log2 domain
   float q[HD], o[HD];
@@ -115,9 +118,8 @@ __global__ __launch_bounds__(kThreads) void attend_f32_kernel(AttendArgs args, i
           size_t off;
           if (k < mem_rows) {
             const int e = k / N;
-            const char* slot = args.kv_layer_base + size_t(order_s[e]) * args.slot_stride;
-            kb = slot;
-            vb = slot + args.v_offset;
+            kb = args.k_base + size_t(order_s[2 * e]) * args.k_stride;
+            vb = args.v_base + size_t(order_s[2 * e + 1]) * args.v_stride;
             off = size_t(k - e * N);
           } else {
             kb = static_cast<const char*>(args.k_cur);
@@ -267,7 +269,7 @@ hipError_t launch_f32(F32Kernel kernel, F32Combine combine, std::once_flag& attr
   if (q_tiles64 * a.heads > int64_t(0x7fffffff)) return hipErrorInvalidValue;
   const int q_tiles = int(q_tiles64);
   const int total = q_tiles * a.heads;
-  const size_t shmem = size_t(a.n_entries) * sizeof(int32_t);  // slot table; tile buffers are static
+  const size_t shmem = size_t(a.n_entries) * 2 * sizeof(int32_t);  // entry tables; tile buffers are static
   if (shmem > 32 * 1024) return hipErrorInvalidValue;
   const int64_t lk = a.n_entries * a.tokens_per_block + a.cur_tokens;
   const int n_tiles = int((lk + kTile - 1) / kTile);

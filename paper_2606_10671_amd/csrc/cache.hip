@@ -10,10 +10,27 @@
 
 #include <mutex>
 #include <new>
+#include <vector>
 
 #include "fademem_internal.h"
 
 using namespace fademem;
+
+namespace {
+
+// Host replay of the memory's metadata and slot table.  The device decides
+// every consolidation itself; the host replays the same steps on the same
+// integers (Alg. S1 with the schedule of select_pair, the slot bookkeeping
+// of the kernels) so that it knows, without reading anything back, which
+// slots are free (the addresses of staged frames) and which entries changed
+// (the re-indexed K views).  fademem_verify and serialize mode compare it
+// with the device state.
+struct Mirror {
+  std::vector<int64_t> first, pos_sum, span;  // held entries, oldest first
+  std::vector<int32_t> order;                 // logical -> slot, all slots
+};
+
+}  // namespace
 
 struct fademem_cache {
   fademem_config cfg;
@@ -26,6 +43,13 @@ struct fademem_cache {
   bool any_inserted;
   bool serialize;       // FADEMEM_SERIALIZE set at creation: every call waits for its work and checks it
   int last_hip_error;
+  Mirror mirror;
+  // Re-indexed K views (rope_pairs > 0): view position i of layer l holds
+  // the rotated K of the entry covering [view_first, view_first + view_span)
+  // (span 0: nothing valid).  An entry's covered range fixes its contents
+  // for the life of a cache: positions strictly increase and ranges only
+  // grow by merging.
+  std::vector<int64_t> view_first, view_span;
 };
 
 namespace {
@@ -36,6 +60,8 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 // End of an asynchronous call: in serialize mode (a debugging aid), wait for
 // the call's work and report a failure at the call that caused it.
+int verify_mirror(fademem_cache* c, void* stream);
+
 int finish(fademem_cache* c, void* stream) {
   if (!c->serialize) return FADEMEM_OK;
   hipError_t e = hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream));
@@ -44,7 +70,7 @@ int finish(fademem_cache* c, void* stream) {
     c->last_hip_error = int(e);
     return FADEMEM_EHIP;
   }
-  return FADEMEM_OK;
+  return verify_mirror(c, stream);
 }
 
 int hip_fail(fademem_cache* c, hipError_t e) {
@@ -379,6 +405,10 @@ __global__ __launch_bounds__(256) void consolidate_kernel(ConsolidateArgs a) {
 // (each rounded to the storage type exactly as a lone merge is), and stores
 // each changed entry once.  Frames consumed by a merge of the same update
 // are read from the caller's buffers and never copied into the pool.
+// Staged frames (the zero-copy update) already sit in free pool slots: they
+// enter the plan as slot references, so a frame that survives the update
+// stays where the caller wrote it and one that a merge consumes frees its
+// slot.
 // ---------------------------------------------------------------------------
 
 struct PlanArgs {
@@ -392,6 +422,7 @@ struct PlanArgs {
   int anchor;
   int op;
   int cur;                 // metadata copy read; the other copy is written
+  int staged;              // 1: frame f is already in slot order[n0 + f]
 };
 
 __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
@@ -399,7 +430,7 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
   constexpr int kCap = kMaxBudget + 1;  // entries held at most (M + 1)
   __shared__ int64_t first_s[kCap], pos_s[kCap], span_s[kCap];
   __shared__ int32_t kind_s[kCap], idx_s[kCap];
-  __shared__ int32_t free_s[kCap];
+  __shared__ int32_t free_s[kMaxBudget + kMaxPlanFrames];  // free slots: at most all M + stage_frames
   __shared__ double u_s[kCap], g_s[kCap];
   __shared__ double red_d[4];
   __shared__ int red_i[4];
@@ -416,9 +447,10 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
     kind_s[i] = kRefSlot;
     idx_s[i] = m.order[i];
   }
-  for (int i = a.n0 + tid; i < slots; i += 256) free_s[i - a.n0] = m.order[i];
+  const int skip = a.staged ? a.frames : 0;  // staged frames' slots are not free
+  for (int i = a.n0 + skip + tid; i < slots; i += 256) free_s[i - a.n0 - skip] = m.order[i];
   if (tid == 0) {
-    n_free_s = slots - a.n0;
+    n_free_s = slots - a.n0 - skip;
     plan.n_ar = 0;
     plan.n_out = 0;
   }
@@ -434,12 +466,12 @@ __global__ __launch_bounds__(256) void update_plan_kernel(PlanArgs a) {
   int n = a.n0;
   for (int f = 0; f < a.frames; ++f) {
     const int64_t t = a.first_position + f;
-    if (tid == 0) {  // Append (K_t, V_t, t, 1), its K, V still the caller's frame f
+    if (tid == 0) {  // Append (K_t, V_t, t, 1), its K, V still the caller's frame f (or its staging slot)
       first_s[n] = t;
       pos_s[n] = t;
       span_s[n] = 1;
-      kind_s[n] = kRefFrame;
-      idx_s[n] = f;
+      kind_s[n] = a.staged ? kRefSlot : kRefFrame;
+      idx_s[n] = a.staged ? m.order[a.n0 + f] : f;
     }
     n += 1;
     __syncthreads();
@@ -622,42 +654,37 @@ __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
 // keys are stored without their temporal phase; for attention, entry e is
 // exposed at temporal index e.  This kernel writes entry e's K with pairs
 // k < P rotated by the angle e * w_k, w_k = theta^(-k/P) (fp64, rounded once
-// to the storage type), and its V unchanged, into view slot e, so the
-// attention kernels read the view through an identity slot table.
-// grid = (blocks per plane, entries * 2): y = entry * 2 + kv.
+// to the storage type), into K block e of the layer's view; V is read from
+// the entry's slot as stored.  Only the listed view positions are written
+// (those whose entry changed since the view was last built).
+// grid = (blocks per block, listed positions).
 // ---------------------------------------------------------------------------
+
+constexpr int kMaxViewPos = 64;  // positions per launch
 
 struct RopeViewArgs {
   const char* kv_layer_base;  // pool + kv_offset(layer, 0, 0)
   const int32_t* order;       // logical -> slot
-  char* view;                 // view slot e at view + e * 2 * blk_stride (K, then V)
-  int32_t* view_order;        // identity table written here
+  char* view;                 // the layer's view: K block e at view + e * blk_stride
   size_t slot_stride;         // 2 * blk_stride
   size_t blk_stride;
-  int64_t units;              // 16-byte units per K (or V) block
-  int n_entries;
+  int64_t units;              // 16-byte units per K block
   int head_dim;
   int pairs;                  // P
   double theta;
+  int n_pos;
+  int32_t pos[kMaxViewPos];   // view positions (= logical entries) to write
 };
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void rope_view_kernel(RopeViewArgs a) {
 #pragma clang fp contract(off)
   __shared__ double cs[64], sn[64];
-  const int e = blockIdx.y >> 1, kv = blockIdx.y & 1;
+  const int e = a.pos[blockIdx.y];
   const int tid = threadIdx.x;
-  if (blockIdx.x == 0 && blockIdx.y == 0)
-    for (int i = tid; i < a.n_entries; i += 256) a.view_order[i] = i;
-  const u32x4* src = reinterpret_cast<const u32x4*>(a.kv_layer_base + size_t(a.order[e]) * a.slot_stride +
-                                                    size_t(kv) * a.blk_stride);
-  u32x4* dst = reinterpret_cast<u32x4*>(a.view + size_t(e) * a.slot_stride + size_t(kv) * a.blk_stride);
+  const u32x4* src = reinterpret_cast<const u32x4*>(a.kv_layer_base + size_t(a.order[e]) * a.slot_stride);
+  u32x4* dst = reinterpret_cast<u32x4*>(a.view + size_t(e) * a.blk_stride);
   const int64_t stride = int64_t(gridDim.x) * 256;
-  if (kv == 1) {  // V: unchanged
-    for (int64_t u = int64_t(blockIdx.x) * 256 + tid; u < a.units; u += stride)
-      __builtin_nontemporal_store(__builtin_nontemporal_load(src + u), dst + u);
-    return;
-  }
   if (tid < a.pairs) {
     const double w = pow(a.theta, -double(tid) / double(a.pairs));
     const double ang = double(e) * w;
@@ -754,7 +781,120 @@ bool valid_config(const fademem_config* c) {
   if (c->layers < 1 || c->layers > 4096) return false;
   if (c->rope_pairs < 0 || c->rope_pairs > c->head_dim / 2) return false;
   if (c->rope_pairs > 0 && !(c->rope_theta > 1.0 && c->rope_theta < 1e300)) return false;
+  if (c->stage_frames < 0 || c->stage_frames > kMaxPlanFrames) return false;
   return true;
+}
+
+
+// ---------------------------------------------------------------------------
+// Host replay (Mirror).  Each function repeats, on the host's copy, what the
+// corresponding kernels do to the metadata and the slot table.
+// ---------------------------------------------------------------------------
+
+// select_pair on the host: the same integers, the same fp64 operations.
+int host_select_pair(const std::vector<int64_t>& span, const std::vector<int64_t>& pos_sum, int n, int64_t t,
+                     double beta) {
+#pragma clang fp contract(off)
+  std::vector<double> u(size_t(n > 1 ? n - 1 : 1));
+  for (int i = 0; i < n - 1; ++i) {
+    const double d = double(t * span[i] - pos_sum[i]) / double(span[i]);
+    u[i] = (beta == 1.0) ? d : pow(d, beta);
+  }
+  double gm = INFINITY;
+  for (int i = 0; i < n - 2; ++i) gm = fmin(gm, fabs(u[i + 1] - u[i]));
+  const double tol = 1e-9 * gm;
+  for (int i = 0; i < n - 2; ++i)
+    if (fabs(u[i + 1] - u[i]) - gm <= tol) return i;
+  return 0;
+}
+
+void mirror_reset(fademem_cache* c) {
+  Mirror& m = c->mirror;
+  m.first.clear();
+  m.pos_sum.clear();
+  m.span.clear();
+  m.order.resize(size_t(c->lay.slots));
+  for (int64_t i = 0; i < c->lay.slots; ++i) m.order[size_t(i)] = int32_t(i);
+  const size_t views = c->cfg.rope_pairs > 0 ? size_t(c->cfg.layers) * size_t(c->lay.slots) : 0;
+  c->view_first.assign(views, 0);
+  c->view_span.assign(views, 0);
+}
+
+// insert_kernel: the new entry goes to slot order[count].
+void mirror_insert(Mirror& m, int64_t t) {
+  m.first.push_back(t);
+  m.pos_sum.push_back(t);
+  m.span.push_back(1);
+}
+
+// consolidate_kernel's block 0.
+void mirror_consolidate(fademem_cache* c) {
+  Mirror& m = c->mirror;
+  const int n = int(m.span.size());
+  const int j = host_select_pair(m.span, m.pos_sum, n, c->newest, c->cfg.beta);
+  const bool anchor_pair = c->cfg.anchor && j == 0;
+  const bool select = c->cfg.merge_op == FADEMEM_MERGE_SELECT_NEAREST && !anchor_pair;
+  const int32_t dst = m.order[size_t(j)], src = m.order[size_t(j) + 1];
+  const int64_t s_new = m.span[size_t(j)] + m.span[size_t(j) + 1];
+  m.pos_sum[size_t(j)] = anchor_pair ? m.first[size_t(j)] * s_new : m.pos_sum[size_t(j)] + m.pos_sum[size_t(j) + 1];
+  m.span[size_t(j)] = s_new;
+  m.first.erase(m.first.begin() + j + 1);
+  m.pos_sum.erase(m.pos_sum.begin() + j + 1);
+  m.span.erase(m.span.begin() + j + 1);
+  m.order[size_t(j)] = select ? src : dst;
+  for (int i = j + 1; i < n - 1; ++i) m.order[size_t(i)] = m.order[size_t(i) + 1];
+  m.order[size_t(n) - 1] = select ? dst : src;
+}
+
+// update_plan_kernel (metadata and slots; the data program is not needed).
+void mirror_update(Mirror& m, const fademem_config& cfg, int64_t n_slots, int frames, int64_t first_position,
+                   bool staged) {
+  const int n0 = int(m.span.size());
+  const int slots = int(n_slots);
+  std::vector<int32_t> kind(size_t(n0), kRefSlot), idx(m.order.begin(), m.order.begin() + n0);
+  std::vector<int32_t> free_list;
+  const int skip = staged ? frames : 0;
+  for (int i = n0 + skip; i < slots; ++i) free_list.push_back(m.order[size_t(i)]);
+  int n_ar = 0;
+  for (int f = 0; f < frames; ++f) {
+    const int64_t t = first_position + f;
+    m.first.push_back(t);
+    m.pos_sum.push_back(t);
+    m.span.push_back(1);
+    kind.push_back(staged ? kRefSlot : kRefFrame);
+    idx.push_back(staged ? m.order[size_t(n0 + f)] : f);
+    const int n = int(m.span.size());
+    if (n <= cfg.budget) continue;
+    const int j = host_select_pair(m.span, m.pos_sum, n, t, cfg.beta);
+    const bool anchor_pair = cfg.anchor && j == 0;
+    const bool select = cfg.merge_op == FADEMEM_MERGE_SELECT_NEAREST && !anchor_pair;
+    const int64_t s_new = m.span[size_t(j)] + m.span[size_t(j) + 1];
+    int32_t nk, ni;
+    if (anchor_pair || select) {
+      const int keep = anchor_pair ? j : j + 1, drop = anchor_pair ? j + 1 : j;
+      nk = kind[size_t(keep)];
+      ni = idx[size_t(keep)];
+      if (kind[size_t(drop)] == kRefSlot) free_list.push_back(idx[size_t(drop)]);
+    } else {
+      if (kind[size_t(j)] == kRefSlot) free_list.push_back(idx[size_t(j)]);
+      if (kind[size_t(j) + 1] == kRefSlot) free_list.push_back(idx[size_t(j) + 1]);
+      nk = kRefResult;
+      ni = n_ar++;
+    }
+    m.pos_sum[size_t(j)] = anchor_pair ? m.first[size_t(j)] * s_new : m.pos_sum[size_t(j)] + m.pos_sum[size_t(j) + 1];
+    m.span[size_t(j)] = s_new;
+    kind[size_t(j)] = nk;
+    idx[size_t(j)] = ni;
+    m.first.erase(m.first.begin() + j + 1);
+    m.pos_sum.erase(m.pos_sum.begin() + j + 1);
+    m.span.erase(m.span.begin() + j + 1);
+    kind.erase(kind.begin() + j + 1);
+    idx.erase(idx.begin() + j + 1);
+  }
+  const int n = int(m.span.size());
+  size_t next = 0;
+  for (int i = 0; i < n; ++i) m.order[size_t(i)] = kind[size_t(i)] == kRefSlot ? idx[size_t(i)] : free_list[next++];
+  for (int i = n; i < slots; ++i) m.order[size_t(i)] = free_list[next++];
 }
 
 }  // namespace
@@ -764,7 +904,7 @@ namespace fademem {
 int compute_layout(const fademem_config* cfg, Layout* lay) {
   if (!valid_config(cfg)) return FADEMEM_EINVAL;
   Layout L{};
-  L.slots = cfg->budget + 1;
+  L.slots = cfg->budget + (cfg->stage_frames > 1 ? cfg->stage_frames : 1);
   size_t off = round_up(sizeof(DevHeader), 256);
   for (int c = 0; c < 2; ++c) {
     L.off_first[c] = off;   off = round_up(off + 8 * size_t(L.slots), 256);
@@ -784,14 +924,44 @@ int compute_layout(const fademem_config* cfg, Layout* lay) {
   L.off_ws = L.meta_bytes + size_t(cfg->layers) * size_t(L.slots) * 2 * L.blk_stride;
   L.ws_bytes = cfg->dtype == FADEMEM_BF16 ? attend_ws_bytes(cfg->head_dim) : f32_ws_bytes(cfg->head_dim);
   L.off_view = round_up(L.off_ws + L.ws_bytes, 256);
-  L.view_bytes = cfg->rope_pairs > 0 ? size_t(cfg->budget) * 2 * L.blk_stride + round_up(4 * size_t(cfg->budget), 256)
-                                     : 0;
+  // One K block per slot and layer: every entry the memory can expose
+  // (M + 1 after an insert, or M plus the staged frames).
+  L.view_bytes = cfg->rope_pairs > 0 ? size_t(cfg->layers) * size_t(L.slots) * L.blk_stride : 0;
   L.total = L.off_view + L.view_bytes;
   *lay = L;
   return FADEMEM_OK;
 }
 
 }  // namespace fademem
+
+namespace {
+
+// Compare the host replay with the device's current metadata copy
+// (synchronises the stream).
+int verify_mirror(fademem_cache* c, void* stream) {
+  hipError_t e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(c, e);
+  const Mirror& m = c->mirror;
+  const size_t n = size_t(c->count);
+  if (m.span.size() != n) return FADEMEM_EINTERNAL;
+  std::vector<int64_t> buf(n);
+  const std::vector<int64_t>* want[3] = {&m.first, &m.pos_sum, &m.span};
+  const size_t offs[3] = {c->lay.off_first[c->cur], c->lay.off_pos_sum[c->cur], c->lay.off_span[c->cur]};
+  for (int a = 0; a < 3; ++a) {
+    if (n == 0) break;
+    if ((e = hipMemcpy(buf.data(), c->pool + offs[a], n * sizeof(int64_t), hipMemcpyDeviceToHost)) != hipSuccess)
+      return hip_fail(c, e);
+    if (buf != *want[a]) return FADEMEM_EINTERNAL;
+  }
+  std::vector<int32_t> ord(size_t(c->lay.slots));
+  if ((e = hipMemcpy(ord.data(), c->pool + c->lay.off_order[c->cur], ord.size() * sizeof(int32_t),
+                     hipMemcpyDeviceToHost)) != hipSuccess)
+    return hip_fail(c, e);
+  if (ord != m.order) return FADEMEM_EINTERNAL;
+  return FADEMEM_OK;
+}
+
+}  // namespace
 
 // ---------------------------------------------------------------------------
 // C ABI
@@ -807,6 +977,7 @@ const char* fademem_strerror(int code) {
     case FADEMEM_ENOMEM: return "device pool too small";
     case FADEMEM_EHIP: return "HIP runtime or launch error";
     case FADEMEM_EUNSUPPORTED: return "not supported by this build";
+    case FADEMEM_EINTERNAL: return "host replay of the memory state disagrees with the device";
     default: return "unknown error";
   }
 }
@@ -842,6 +1013,15 @@ int fademem_cache_create(const fademem_config* cfg, void* dev_pool, size_t pool_
   const char* ser = getenv("FADEMEM_SERIALIZE");
   c->serialize = ser && ser[0] && strcmp(ser, "0") != 0;
   c->last_hip_error = 0;
+  try {
+    mirror_reset(c);
+    c->mirror.first.reserve(size_t(L.slots));
+    c->mirror.pos_sum.reserve(size_t(L.slots));
+    c->mirror.span.reserve(size_t(L.slots));
+  } catch (...) {
+    delete c;
+    return FADEMEM_ENOMEM;
+  }
   (void)hipGetLastError();
   const unsigned blocks = unsigned((L.slots + 255) / 256);
   hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, as_stream(stream), c->pool, L);
@@ -904,6 +1084,7 @@ int fademem_insert(fademem_cache* c, const void* const* k, const void* const* v,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(c, e);
   }
+  mirror_insert(c->mirror, position);  // capacity reserved at creation: no allocation
   c->count += 1;
   c->inserted += 1;
   c->newest = position;
@@ -937,21 +1118,24 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   hipLaunchKernelGGL(kernel, dim3(blocks), dim3(256), 0, as_stream(stream), a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(c, e);
+  mirror_consolidate(c);  // erases in place: no allocation
   c->cur ^= 1;
   c->count -= 1;
   return finish(c, stream);
 }
 
-int fademem_update(fademem_cache* c, const void* const* k, const void* const* v, int64_t frames,
-                   int64_t first_position, void* stream) {
-  if (!c || !k || !v) return FADEMEM_EINVAL;
-  if (frames < 1 || frames > kMaxTokens) return FADEMEM_EINVAL;
+}  // extern "C"
+
+namespace {
+
+// The F updates of a chunk (fademem_update, fademem_update_staged).  k, v:
+// the caller's chunk per layer, or NULL when the frames are staged in the
+// slots order[count + f].
+int update_impl(fademem_cache* c, const void* const* k, const void* const* v, int64_t frames, int64_t first_position,
+                bool staged, void* stream) {
   // Every position f, first_position <= f <= first_position + frames - 1, must satisfy |f| < 2^40.
   if (first_position <= -kMaxPosition || first_position > kMaxPosition - frames) return FADEMEM_EINVAL;
   const int layers = c->cfg.layers;
-  for (int l = 0; l < layers; ++l) {
-    if (!k[l] || !v[l] || !aligned(k[l], 16) || !aligned(v[l], 16)) return FADEMEM_EINVAL;
-  }
   if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
   if (c->any_inserted && first_position <= c->newest) return FADEMEM_ESTATE;
   // t*s_i and first*s_i must stay exact in int64 (as for fademem_insert).
@@ -961,6 +1145,21 @@ int fademem_update(fademem_cache* c, const void* const* k, const void* const* v,
     const int64_t a1 = last < 0 ? -last : last;
     const unsigned __int128 mag = (unsigned __int128)(a0 > a1 ? a0 : a1) + 1;
     if (mag * (unsigned __int128)(c->inserted + frames) >= ((unsigned __int128)1 << 62)) return FADEMEM_ESTATE;
+  }
+  // The host replay of the whole call, committed once everything is enqueued.
+  Mirror next;
+  try {
+    next = c->mirror;
+    for (int64_t f0 = 0; f0 < frames; f0 += kMaxPlanFrames) {
+      const int nf = int((frames - f0) < kMaxPlanFrames ? (frames - f0) : kMaxPlanFrames);
+      mirror_update(next, c->cfg, c->lay.slots, nf, first_position + f0, staged);
+    }
+    // Inserts push onto these without allocating.
+    next.first.reserve(size_t(c->lay.slots));
+    next.pos_sum.reserve(size_t(c->lay.slots));
+    next.span.reserve(size_t(c->lay.slots));
+  } catch (...) {
+    return FADEMEM_ENOMEM;
   }
   (void)hipGetLastError();
   const int64_t units = int64_t(c->lay.blk_bytes / 16);
@@ -982,6 +1181,7 @@ int fademem_update(fademem_cache* c, const void* const* k, const void* const* v,
     pa.anchor = c->cfg.anchor;
     pa.op = c->cfg.merge_op;
     pa.cur = c->cur;
+    pa.staged = staged ? 1 : 0;
     hipLaunchKernelGGL(update_plan_kernel, dim3(1), dim3(256), 0, as_stream(stream), pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(c, e);
@@ -989,9 +1189,11 @@ int fademem_update(fademem_cache* c, const void* const* k, const void* const* v,
       const int nl = (layers - l0) < kMaxLayersPerLaunch ? (layers - l0) : kMaxLayersPerLaunch;
       UpdateDataArgs da;
       memset(&da, 0, sizeof(da));
-      for (int l = 0; l < nl; ++l) {
-        da.k[l] = static_cast<const char*>(k[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
-        da.v[l] = static_cast<const char*>(v[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
+      if (!staged) {
+        for (int l = 0; l < nl; ++l) {
+          da.k[l] = static_cast<const char*>(k[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
+          da.v[l] = static_cast<const char*>(v[l0 + l]) + size_t(f0) * c->lay.blk_bytes;
+        }
       }
       da.pool = c->pool;
       da.lay = c->lay;
@@ -1012,69 +1214,164 @@ int fademem_update(fademem_cache* c, const void* const* k, const void* const* v,
     c->newest = first_position + f0 + nf - 1;
     c->any_inserted = true;
   }
+  c->mirror = std::move(next);
   return finish(c, stream);
 }
 
-int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, const void* k_cur,
-                   const void* v_cur, int64_t cur_tokens, float scale, void* out, float* lse, void* stream) {
-  if (!c) return FADEMEM_EINVAL;
+// Rebuild the stale positions of layer `layer`'s re-indexed K view: the
+// first `held` positions are memory entries (rebuilt when the entry's
+// covered range changed since the last build), the `staged` after them are
+// staged frames (always rebuilt: their contents are the caller's).
+int refresh_view(fademem_cache* c, int32_t layer, int held, int staged, void* stream) {
+  const size_t base = size_t(layer) * size_t(c->lay.slots);
+  std::vector<int32_t> todo;
+  try {
+    todo.reserve(size_t(held + staged));
+  } catch (...) {
+    return FADEMEM_ENOMEM;
+  }
+  for (int i = 0; i < held; ++i) {
+    if (c->view_first[base + i] != c->mirror.first[size_t(i)] || c->view_span[base + i] != c->mirror.span[size_t(i)])
+      todo.push_back(i);
+  }
+  for (int i = held; i < held + staged; ++i) todo.push_back(i);
+  if (todo.empty()) return FADEMEM_OK;
+  RopeViewArgs r;
+  r.kv_layer_base = c->pool + kv_offset(c->lay, layer, 0, 0);
+  r.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order[c->cur]);
+  r.view = c->pool + c->lay.off_view + base * c->lay.blk_stride;
+  r.slot_stride = 2 * c->lay.blk_stride;
+  r.blk_stride = c->lay.blk_stride;
+  r.units = int64_t(c->lay.blk_bytes / 16);
+  r.head_dim = c->cfg.head_dim;
+  r.pairs = c->cfg.rope_pairs;
+  r.theta = c->cfg.rope_theta;
+  auto vk = c->cfg.dtype == FADEMEM_BF16 ? rope_view_kernel<true> : rope_view_kernel<false>;
+  for (size_t p0 = 0; p0 < todo.size(); p0 += kMaxViewPos) {
+    const int np = int(todo.size() - p0 < size_t(kMaxViewPos) ? todo.size() - p0 : size_t(kMaxViewPos));
+    r.n_pos = np;
+    for (int i = 0; i < np; ++i) r.pos[i] = todo[p0 + i];
+    const dim3 grid(stream_blocks_per_plane(reinterpret_cast<const void*>(vk), unsigned(np), r.units, 4),
+                    unsigned(np));
+    hipLaunchKernelGGL(vk, grid, dim3(256), 0, as_stream(stream), r);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(c, e);
+  }
+  for (int i = 0; i < held; ++i) {
+    c->view_first[base + i] = c->mirror.first[size_t(i)];
+    c->view_span[base + i] = c->mirror.span[size_t(i)];
+  }
+  for (int i = held; i < held + staged; ++i) c->view_span[base + i] = 0;  // rebuilt on every use
+  return FADEMEM_OK;
+}
+
+// Attention over [memory || staged frames || current chunk] (the staged
+// frames are exposed as entries after the memory's).
+int attend_impl(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, const void* k_cur,
+                const void* v_cur, int64_t cur_tokens, int64_t staged, float scale, void* out, float* lse,
+                void* stream) {
   if (layer < 0 || layer >= c->cfg.layers) return FADEMEM_EINVAL;
   if (q_tokens < 0 || q_tokens > kMaxTokens || cur_tokens < 0 || cur_tokens > kMaxTokens) return FADEMEM_EINVAL;
   if (q_tokens == 0) return FADEMEM_OK;
   if (!q || !out || !aligned(q, 16) || !aligned(out, 16)) return FADEMEM_EINVAL;
   if (lse && !aligned(lse, 4)) return FADEMEM_EINVAL;
   if (cur_tokens > 0 && (!k_cur || !v_cur || !aligned(k_cur, 16) || !aligned(v_cur, 16))) return FADEMEM_EINVAL;
-  if (c->count == 0 && cur_tokens == 0) return FADEMEM_EINVAL;  // no keys at all
-  const double total_keys = double(c->count) * double(c->cfg.tokens_per_block) + double(cur_tokens);
+  const int64_t entries = c->count + staged;
+  if (entries == 0 && cur_tokens == 0) return FADEMEM_EINVAL;  // no keys at all
+  const double total_keys = double(entries) * double(c->cfg.tokens_per_block) + double(cur_tokens);
   if (total_keys > double(kMaxTokens)) return FADEMEM_EINVAL;
   if (!(scale >= 0.0f) || isinf(scale)) return FADEMEM_EINVAL;
   AttendArgs a;
   a.q = q;
   a.out = out;
   a.lse = lse;
-  a.kv_layer_base = c->pool + kv_offset(c->lay, layer, 0, 0);
-  a.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order[c->cur]);
+  a.k_base = c->pool + kv_offset(c->lay, layer, 0, 0);
+  a.k_order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order[c->cur]);
+  a.k_stride = 2 * c->lay.blk_stride;
+  a.v_base = a.k_base + c->lay.blk_stride;
+  a.v_order = a.k_order;
+  a.v_stride = a.k_stride;
   a.k_cur = k_cur;
   a.v_cur = v_cur;
-  a.n_entries = c->count;
+  a.n_entries = entries;
   a.tokens_per_block = c->cfg.tokens_per_block;
   a.cur_tokens = cur_tokens;
   a.q_tokens = q_tokens;
-  a.slot_stride = 2 * c->lay.blk_stride;
-  a.v_offset = c->lay.blk_stride;
   a.ws = reinterpret_cast<float*>(c->pool + c->lay.off_ws);
   a.heads = c->cfg.heads;
   a.head_dim = c->cfg.head_dim;
   a.scale = scale > 0.0f ? scale : 1.0f / sqrtf(float(c->cfg.head_dim));
   (void)hipGetLastError();
-  if (c->cfg.rope_pairs > 0 && c->count > 0) {
-    // Expose the memory re-indexed: a rotated K (and copied V) view of the
-    // held entries, read through an identity slot table.
-    RopeViewArgs r;
-    r.kv_layer_base = a.kv_layer_base;
-    r.order = a.order;
-    r.view = c->pool + c->lay.off_view;
-    r.view_order = reinterpret_cast<int32_t*>(c->pool + c->lay.off_view + size_t(c->cfg.budget) * 2 * c->lay.blk_stride);
-    r.slot_stride = 2 * c->lay.blk_stride;
-    r.blk_stride = c->lay.blk_stride;
-    r.units = int64_t(c->lay.blk_bytes / 16);
-    r.n_entries = int(c->count);
-    r.head_dim = c->cfg.head_dim;
-    r.pairs = c->cfg.rope_pairs;
-    r.theta = c->cfg.rope_theta;
-    auto vk = c->cfg.dtype == FADEMEM_BF16 ? rope_view_kernel<true> : rope_view_kernel<false>;
-    const unsigned planes = unsigned(2 * c->count);
-    const dim3 grid(stream_blocks_per_plane(reinterpret_cast<const void*>(vk), planes, r.units, 4), planes);
-    hipLaunchKernelGGL(vk, grid, dim3(256), 0, as_stream(stream), r);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(c, e);
-    a.kv_layer_base = r.view;
-    a.order = r.view_order;
+  if (c->cfg.rope_pairs > 0 && entries > 0) {
+    // Expose the memory re-indexed: keys from the layer's rotated K view
+    // (entry e at view position e), values from the slots as stored.
+    const int rc = refresh_view(c, layer, int(c->count), int(staged), stream);
+    if (rc) return rc;
+    a.k_base = c->pool + c->lay.off_view + size_t(layer) * size_t(c->lay.slots) * c->lay.blk_stride;
+    a.k_order = nullptr;
+    a.k_stride = c->lay.blk_stride;
   }
   hipError_t e = (c->cfg.dtype == FADEMEM_BF16) ? launch_attend_bf16(a, as_stream(stream))
                                                 : launch_attend_f32(a, as_stream(stream));
   if (e != hipSuccess) return hip_fail(c, e);
   return finish(c, stream);
+}
+
+bool chunk_ptrs_ok(const fademem_cache* c, const void* const* k, const void* const* v) {
+  if (!k || !v) return false;
+  for (int l = 0; l < c->cfg.layers; ++l)
+    if (!k[l] || !v[l] || !aligned(k[l], 16) || !aligned(v[l], 16)) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fademem_update(fademem_cache* c, const void* const* k, const void* const* v, int64_t frames,
+                   int64_t first_position, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (frames < 1 || frames > kMaxTokens) return FADEMEM_EINVAL;
+  if (!chunk_ptrs_ok(c, k, v)) return FADEMEM_EINVAL;
+  return update_impl(c, k, v, frames, first_position, false, stream);
+}
+
+int fademem_stage(fademem_cache* c, int64_t frames, void** k, void** v) {
+  if (!c || !k || !v) return FADEMEM_EINVAL;
+  if (frames < 1 || frames > c->cfg.stage_frames) return FADEMEM_EINVAL;
+  if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
+  for (int l = 0; l < c->cfg.layers; ++l)
+    for (int64_t f = 0; f < frames; ++f) {
+      const int32_t slot = c->mirror.order[size_t(c->count + f)];
+      k[size_t(l) * size_t(frames) + size_t(f)] = c->pool + kv_offset(c->lay, l, slot, 0);
+      v[size_t(l) * size_t(frames) + size_t(f)] = c->pool + kv_offset(c->lay, l, slot, 1);
+    }
+  return FADEMEM_OK;
+}
+
+int fademem_update_staged(fademem_cache* c, int64_t frames, int64_t first_position, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (frames < 1 || frames > c->cfg.stage_frames) return FADEMEM_EINVAL;
+  return update_impl(c, nullptr, nullptr, frames, first_position, true, stream);
+}
+
+int fademem_attend(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, const void* k_cur,
+                   const void* v_cur, int64_t cur_tokens, float scale, void* out, float* lse, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  return attend_impl(c, layer, q, q_tokens, k_cur, v_cur, cur_tokens, 0, scale, out, lse, stream);
+}
+
+int fademem_attend_staged(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens, int64_t frames,
+                          float scale, void* out, float* lse, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  if (frames < 1 || frames > c->cfg.stage_frames) return FADEMEM_EINVAL;
+  if (c->count > c->cfg.budget) return FADEMEM_ESTATE;
+  return attend_impl(c, layer, q, q_tokens, nullptr, nullptr, 0, frames, scale, out, lse, stream);
+}
+
+int fademem_verify(fademem_cache* c, void* stream) {
+  if (!c) return FADEMEM_EINVAL;
+  return verify_mirror(c, stream);
 }
 
 int fademem_get_state(fademem_cache* c, int64_t* count, int64_t* first, int64_t* span, int64_t* pos_sum,
@@ -1158,6 +1455,17 @@ int fademem_set_state(fademem_cache* c, int64_t count, const int64_t* first, con
         return hip_fail(c, e);
     }
   if ((e = hipStreamSynchronize(s)) != hipSuccess) return hip_fail(c, e);
+  try {
+    mirror_reset(c);
+    c->mirror.first.assign(first, first + count);
+    c->mirror.span.assign(span, span + count);
+    c->mirror.pos_sum.assign(pos_sum, pos_sum + count);
+    c->mirror.first.reserve(size_t(c->lay.slots));
+    c->mirror.pos_sum.reserve(size_t(c->lay.slots));
+    c->mirror.span.reserve(size_t(c->lay.slots));
+  } catch (...) {
+    return FADEMEM_ENOMEM;
+  }
   c->cur = 0;
   c->count = count;
   c->newest = newest;

@@ -28,9 +28,10 @@ constexpr int kAttnThreads = 512;        // threads per workgroup (8 waves)
 constexpr int kAttnQueries = 256;        // queries per workgroup (32 per wave)
 constexpr int kSkMaxGroups = 256;        // workgroups of one launch at most (one per CU)
 __host__ __device__ constexpr size_t attend_slot_floats(int head_dim) {
-  // O of every query, then the row max and the partial row sum of every
+  // O of every query, then the row max, the partial row sum of the rounded
+  // weights and that of the unrounded weights (kept for the LSE) of every
   // (thread, 32-query block).
-  return size_t(kAttnQueries) * size_t(head_dim) + 4 * size_t(kAttnQueries);
+  return size_t(kAttnQueries) * size_t(head_dim) + 6 * size_t(kAttnQueries);
 }
 __host__ __device__ constexpr size_t attend_ws_bytes(int head_dim) {
   return 2 * size_t(kSkMaxGroups) * attend_slot_floats(head_dim) * sizeof(float);
@@ -77,10 +78,10 @@ struct UpdatePlan {
 // many blocks of the merge kernel that all derive the schedule decision
 // from the metadata never race with the block that updates it.  Arrays are
 // indexed by logical entry (0 = oldest); order[] maps logical entry -> KV
-// slot and is a permutation of 0..M whose first `count` elements are the
-// live entries' slots (the rest are free), so compaction never moves KV.
+// slot and is a permutation of the slots whose first `count` elements are
+// the live entries' slots (the rest are free), so compaction never moves KV.
 struct Layout {
-  int64_t slots;          // M + 1
+  int64_t slots;          // M + max(1, stage_frames)
   size_t off_first[2];    // int64[slots]
   size_t off_pos_sum[2];  // int64[slots]
   size_t off_span[2];     // int64[slots]
@@ -94,7 +95,7 @@ struct Layout {
   size_t row_elems;       // H*D: elements per token row
   size_t off_ws;          // attention scratch, after the KV region
   size_t ws_bytes;        // attend_ws_bytes(D) for bf16, f32_ws_bytes(D) for fp32
-  size_t off_view;        // RoPE view: M slots of K (rotated) and V, then an identity slot table
+  size_t off_view;        // RoPE views: per layer, one rotated K block per view position (= logical entry)
   size_t view_bytes;      // 0 when rope_pairs = 0
   size_t total;           // off_view + view_bytes
 };
@@ -107,23 +108,29 @@ __host__ __device__ inline size_t kv_offset(const Layout& lay, int64_t layer, in
 }
 
 // Attention launchers (attend_bf16.hip, attend_f32.hip).  All pointers are
-// device pointers; `entry_k0` is layer's KV region base (slot 0, K) and the
-// slot of logical entry e is order[e]; slot s's K block starts at
-// entry_k0 + s*2*blk_stride bytes and its V block blk_stride bytes later.
+// device pointers.  The exposed keys are entries e = 0..n_entries-1 of N
+// rows each, then the current chunk's cur_tokens rows.  Entry e's K rows
+// start at k_base + k_order[e] * k_stride (k_order NULL: the identity) and
+// its V rows at v_base + v_order[e] * v_stride; a row is [H][D].  For the
+// memory as stored, k_base is the layer's slot 0 K block, v_base its V
+// block, both orders the slot table and both strides the slot stride; a
+// re-indexed K view or staged frames only change the tables.
 struct AttendArgs {
   const void* q;
   void* out;
   float* lse;
-  const char* kv_layer_base;  // pool + kv_offset(layer, 0, 0)
-  const int32_t* order;       // logical -> slot
+  const char* k_base;
+  const int32_t* k_order;     // logical -> K block index (NULL: e)
+  size_t k_stride;
+  const char* v_base;
+  const int32_t* v_order;     // logical -> V block index
+  size_t v_stride;
   const void* k_cur;
   const void* v_cur;
   int64_t n_entries;          // entries exposed from memory
   int64_t tokens_per_block;   // N
   int64_t cur_tokens;         // rows of the current chunk
   int64_t q_tokens;
-  size_t slot_stride;         // bytes between consecutive slots' K blocks (2*blk_stride)
-  size_t v_offset;            // bytes from a slot's K block to its V block
   float* ws;                  // attention scratch: 2*kSkMaxGroups slots (bf16), kF32MaxParts slots (fp32)
   int heads;
   int head_dim;

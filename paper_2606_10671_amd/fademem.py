@@ -20,6 +20,7 @@ FADEMEM_ESTATE = -2
 FADEMEM_ENOMEM = -3
 FADEMEM_EHIP = -4
 FADEMEM_EUNSUPPORTED = -5
+FADEMEM_EINTERNAL = -6
 FADEMEM_F32 = 0
 FADEMEM_BF16 = 1
 FADEMEM_MERGE_SQRT_SPAN = 0
@@ -33,7 +34,8 @@ EXPORTED = (
     "fademem_pool_bytes", "fademem_cache_create", "fademem_cache_destroy", "fademem_insert",
     "fademem_consolidate", "fademem_update", "fademem_attend", "fademem_count", "fademem_get_state",
     "fademem_entry_kv", "fademem_set_state", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
-    "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr",
+    "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr", "fademem_stage",
+    "fademem_update_staged", "fademem_attend_staged", "fademem_verify",
 )
 
 
@@ -50,6 +52,7 @@ class fademem_config(ctypes.Structure):
         ("layers", ctypes.c_int32),
         ("rope_pairs", ctypes.c_int32),
         ("rope_theta", ctypes.c_double),
+        ("stage_frames", ctypes.c_int32),
     ]
 
 
@@ -109,6 +112,11 @@ def lib() -> ctypes.CDLL:
                                                    P(ctypes.c_size_t)]
     L.fademem_spectral_corr.argtypes = [c_void_p, c_int64, c_int64, c_int32, c_int32, c_void_p, c_int32, c_int64,
                                         c_void_p, ctypes.c_size_t, c_void_p, c_void_p]
+    L.fademem_stage.argtypes = [c_void_p, c_int64, P(c_void_p), P(c_void_p)]
+    L.fademem_update_staged.argtypes = [c_void_p, c_int64, c_int64, c_void_p]
+    L.fademem_attend_staged.argtypes = [c_void_p, c_int32, c_void_p, c_int64, c_int64, ctypes.c_float, c_void_p,
+                                        c_void_p, c_void_p]
+    L.fademem_verify.argtypes = [c_void_p, c_void_p]
     L.fademem_last_hip_error.argtypes = [c_void_p]
     for name in EXPORTED:
         if name != "fademem_strerror":
@@ -126,10 +134,10 @@ def _ok(rc: int, where: str) -> None:
 def make_config(budget: int, heads: int, head_dim: int, tokens_per_block: int, beta: float = 0.3,
                 anchor: bool = True, dtype: int = FADEMEM_BF16, layers: int = 1,
                 merge_op: int = FADEMEM_MERGE_SQRT_SPAN, rope_pairs: int = 0,
-                rope_theta: float = 10000.0) -> fademem_config:
+                rope_theta: float = 10000.0, stage_frames: int = 0) -> fademem_config:
     return fademem_config(budget=budget, heads=heads, head_dim=head_dim, tokens_per_block=tokens_per_block,
                           beta=beta, anchor=int(anchor), merge_op=merge_op, dtype=dtype, layers=layers,
-                          rope_pairs=rope_pairs, rope_theta=rope_theta)
+                          rope_pairs=rope_pairs, rope_theta=rope_theta, stage_frames=stage_frames)
 
 
 # -- the C calls, same names ---------------------------------------------------
@@ -178,6 +186,30 @@ def fademem_attend(handle: int, layer: int, q_ptr: int, q_tokens: int, k_cur_ptr
                              ctypes.c_void_p(k_cur_ptr), ctypes.c_void_p(v_cur_ptr), cur_tokens,
                              ctypes.c_float(scale), ctypes.c_void_p(out_ptr), ctypes.c_void_p(lse_ptr),
                              ctypes.c_void_p(stream)), "fademem_attend")
+
+
+def fademem_stage(handle: int, layers: int, frames: int):
+    """Device addresses of the staging slots: ([k per (layer, frame)], [v ...]), layer-major."""
+    n = layers * frames
+    ka, va = (ctypes.c_void_p * n)(), (ctypes.c_void_p * n)()
+    _ok(lib().fademem_stage(ctypes.c_void_p(handle), frames, ka, va), "fademem_stage")
+    return [int(x) for x in ka], [int(x) for x in va]
+
+
+def fademem_update_staged(handle: int, frames: int, first_position: int, stream: int = 0) -> None:
+    _ok(lib().fademem_update_staged(ctypes.c_void_p(handle), frames, first_position, ctypes.c_void_p(stream)),
+        "fademem_update_staged")
+
+
+def fademem_attend_staged(handle: int, layer: int, q_ptr: int, q_tokens: int, frames: int, scale: float,
+                          out_ptr: int, lse_ptr: int = 0, stream: int = 0) -> None:
+    _ok(lib().fademem_attend_staged(ctypes.c_void_p(handle), layer, ctypes.c_void_p(q_ptr), q_tokens, frames,
+                                    ctypes.c_float(scale), ctypes.c_void_p(out_ptr), ctypes.c_void_p(lse_ptr),
+                                    ctypes.c_void_p(stream)), "fademem_attend_staged")
+
+
+def fademem_verify(handle: int, stream: int = 0) -> None:
+    _ok(lib().fademem_verify(ctypes.c_void_p(handle), ctypes.c_void_p(stream)), "fademem_verify")
 
 
 def fademem_count(handle: int) -> int:
@@ -267,7 +299,7 @@ class Cache:
 
     def __init__(self, budget: int, heads: int, head_dim: int, tokens_per_block: int, beta: float = 0.3,
                  anchor: bool = True, dtype=None, layers: int = 1, device=None, merge_op: str = "sqrt_span",
-                 rope_pairs: int = 0, rope_theta: float = 10000.0):
+                 rope_pairs: int = 0, rope_theta: float = 10000.0, stage_frames: int = 0):
         import torch
         dtype = torch.bfloat16 if dtype is None else dtype
         if dtype not in (torch.float32, torch.bfloat16):
@@ -277,7 +309,8 @@ class Cache:
         self.torch_dtype = dtype
         self.cfg = make_config(budget, heads, head_dim, tokens_per_block, beta, anchor,
                                FADEMEM_BF16 if dtype == torch.bfloat16 else FADEMEM_F32, layers,
-                               merge_op=MERGE_OPS[merge_op], rope_pairs=rope_pairs, rope_theta=rope_theta)
+                               merge_op=MERGE_OPS[merge_op], rope_pairs=rope_pairs, rope_theta=rope_theta,
+                               stage_frames=stage_frames)
         self.device = torch.device("cuda") if device is None else torch.device(device)
         self.pool_bytes = fademem_pool_bytes(self.cfg)
         self.pool = torch.empty(self.pool_bytes, dtype=torch.uint8, device=self.device)
@@ -342,6 +375,43 @@ class Cache:
                        self._stream(stream))
         return out
 
+    def _block_view(self, ptr: int):
+        import torch
+        base = self.pool.data_ptr()
+        elt = 2 if self.torch_dtype == torch.bfloat16 else 4
+        n = self.cfg.tokens_per_block * self.cfg.heads * self.cfg.head_dim
+        shape = (self.cfg.tokens_per_block, self.cfg.heads, self.cfg.head_dim)
+        return self.pool[ptr - base: ptr - base + n * elt].view(self.torch_dtype).view(shape)
+
+    def stage(self, frames: int):
+        """Staging blocks for the zero-copy update: per layer, a list of
+        `frames` (K, V) [N][H][D] views of free pool slots to write the chunk's
+        frames into (valid until the next update)."""
+        kp, vp = fademem_stage(self.handle, self.cfg.layers, frames)
+        return [[(self._block_view(kp[l * frames + f]), self._block_view(vp[l * frames + f]))
+                 for f in range(frames)] for l in range(self.cfg.layers)]
+
+    def update_staged(self, frames: int, first_position: int, stream=None):
+        fademem_update_staged(self.handle, frames, first_position, self._stream(stream))
+
+    def attend_staged(self, q, frames: int, layer: int = 0, scale: float = 0.0, out=None, lse=None, stream=None):
+        """Attention over [memory || the staged frames]."""
+        import torch
+        self._check(q, None, "q")
+        if out is None:
+            out = torch.empty_like(q)
+        self._check(out, q.shape[0], "out")
+        if lse is not None and (lse.dtype != torch.float32 or not lse.is_contiguous()
+                                or tuple(lse.shape) != (self.cfg.heads, q.shape[0])):
+            raise ValueError("lse: expected a contiguous float32 [heads][q_tokens] tensor")
+        fademem_attend_staged(self.handle, layer, q.data_ptr(), q.shape[0], frames, scale, out.data_ptr(),
+                              0 if lse is None else lse.data_ptr(), self._stream(stream))
+        return out
+
+    def verify(self, stream=None):
+        """Check the host replay of the memory against the device (synchronises)."""
+        fademem_verify(self.handle, self._stream(stream))
+
     def count(self) -> int:
         return fademem_count(self.handle)
 
@@ -358,13 +428,7 @@ class Cache:
         """Views of logical entry i's K and V (valid until the next update)."""
         import torch
         kp, vp = fademem_entry_kv(self.handle, layer, i, self._stream(stream))
-        base = self.pool.data_ptr()
-        elt = 2 if self.torch_dtype == torch.bfloat16 else 4
-        n = self.cfg.tokens_per_block * self.cfg.heads * self.cfg.head_dim
-        shape = (self.cfg.tokens_per_block, self.cfg.heads, self.cfg.head_dim)
-        k = self.pool[kp - base: kp - base + n * elt].view(self.torch_dtype).view(shape)
-        v = self.pool[vp - base: vp - base + n * elt].view(self.torch_dtype).view(shape)
-        return k, v
+        return self._block_view(kp), self._block_view(vp)
 
     def snapshot(self, stream=None) -> dict:
         """Checkpoint: the metadata and device copies of every entry's K and V

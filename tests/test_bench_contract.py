@@ -47,10 +47,22 @@ def test_measured_traffic_is_tied_to_its_workload():
     assert bench.measured_traffic(bench.ATTN_TRAFFIC, "no_such_file.hip", "wan1.3b-1layer") is None
 
 
-def test_budget_override_rejects_an_empty_memory():
-    """`--budget` replaces the workload's M; a budget below one entry is refused before any GPU work."""
+@pytest.mark.parametrize("budget", ["0", "1"])
+def test_budget_override_rejects_a_memory_without_an_eligible_pair(budget):
+    """`--budget` replaces the workload's M; the library needs M >= 2 (one
+    pair besides the newest entry), and bench.py refuses less before any GPU work."""
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--budget", "0"], capture_output=True,
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--budget", budget], capture_output=True,
                        text=True, timeout=300, cwd=root)
     assert r.returncode != 0
-    assert "--budget must be at least 1" in r.stderr
+    assert "--budget must be at least 2" in r.stderr
+
+
+@pytest.mark.parametrize("js,count0,F,M,anchor,op,expect", [
+    ([], 2, 1, 5, True, "sqrt_span", (0, 0)),               # no merge: the staged frame stays in its slot
+    ([1], 2, 1, 2, True, "sqrt_span", (2, 1)),              # frame merged: loaded from its staging slot
+    ([0], 2, 1, 2, True, "sqrt_span", (0, 0)),              # anchor pair: no bytes, the frame stays
+    ([18, 17, 18], 21, 3, 21, True, "sqrt_span", (5, 2)),   # steady state: three merges (one chained), two results kept
+])
+def test_staged_update_block_count(js, count0, F, M, anchor, op, expect):
+    assert bench.fused_block_ios(js, count0, F, M, anchor, op, staged=True) == expect

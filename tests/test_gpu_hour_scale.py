@@ -9,6 +9,12 @@ entry i of layer l must equal rows [l, l + N) of the oracle's entry i, bit
 for bit.  The schedule state (int64 positions, spans, pos_sums) is checked
 against the oracle along the run and at the end, the merge log at the end,
 and attention of the last chunk on sampled query rows of layers 0 and 29.
+
+The run is made three ways: one fademem_insert + fademem_consolidate per
+frame, one fused fademem_update per chunk (the benchmark's path: its plan
+kernel's merge log wraps past its 4096-entry ring and its counters grow to
+14 379 consolidations), and the zero-copy staged update, whose host replay
+of the slot table is checked against the device along the run.
 """
 import numpy as np
 import pytest
@@ -22,17 +28,19 @@ H, D, N, F, M, L, CHUNKS = 12, 128, 1560, 3, 21, 30, 4800
 HEAD = 5
 
 
-def test_hour_scale_thirty_layers():
+@pytest.mark.parametrize("update", ["single", "fused", "staged"])
+def test_hour_scale_thirty_layers(update):
     import torch
     from paper_2606_10671_amd.fademem import Cache
     from paper_2606_10671_amd.synth import TorchWanStream
-    print(f"hour-scale H={H} D={D} N={N} F={F} M={M} layers={L} chunks={CHUNKS}", flush=True)
+    print(f"hour-scale H={H} D={D} N={N} F={F} M={M} layers={L} chunks={CHUNKS} update={update}", flush=True)
     cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=torch.bfloat16,
-                  layers=L)
+                  layers=L, stage_frames=F if update == "staged" else 0)
     blk = N * H * D * 2
-    # Peak cache bytes: M+1 slots per layer of K and V, plus metadata and
-    # the attention scratch.
-    assert (M + 1) * L * 2 * blk <= cache.pool_bytes <= (M + 1) * L * 2 * blk + 128 * 2**20
+    # Peak cache bytes: M+1 slots per layer of K and V (M+F when staging),
+    # plus metadata and the attention scratch.
+    slots = M + (F if update == "staged" else 1)
+    assert slots * L * 2 * blk <= cache.pool_bytes <= slots * L * 2 * blk + 128 * 2**20
     print(f"pool bytes {cache.pool_bytes}", flush=True)
     stream = TorchWanStream(7, N + L - 1, H, D)
     oc = OracleCache(budget=M, beta=0.3, anchor=True, storage="bf16")
@@ -59,13 +67,27 @@ def test_hour_scale_thirty_layers():
                 print(f"last chunk layer {layer}: max-abs {err:.3e} normwise {norm:.3e} lse {lerr:.3e}", flush=True)
                 assert err <= BF16_MAX_ABS and norm <= BF16_NORM_RTOL and lerr <= BF16_LSE_ABS, (layer, err, norm,
                                                                                                 lerr)
+        if update == "single":
+            for f, (k, v) in enumerate(frames):
+                cache.insert([k[layer:layer + N] for layer in range(L)], [v[layer:layer + N] for layer in range(L)],
+                             c * F + f)
+                cache.consolidate()
+        elif update == "fused":
+            cache.update([torch.cat([k[layer:layer + N] for k, _ in frames]) for layer in range(L)],
+                         [torch.cat([v[layer:layer + N] for _, v in frames]) for layer in range(L)], c * F)
+        else:
+            staged = cache.stage(F)
+            for layer in range(L):
+                for f, (k, v) in enumerate(frames):
+                    staged[layer][f][0].copy_(k[layer:layer + N])
+                    staged[layer][f][1].copy_(v[layer:layer + N])
+            cache.update_staged(F, c * F)
         for f, (k, v) in enumerate(frames):
-            t = c * F + f
-            cache.insert([k[layer:layer + N] for layer in range(L)], [v[layer:layer + N] for layer in range(L)], t)
-            cache.consolidate()
-            oc.update(to_np(k[:, HEAD:HEAD + 1]), to_np(v[:, HEAD:HEAD + 1]), t)
+            oc.update(to_np(k[:, HEAD:HEAD + 1]), to_np(v[:, HEAD:HEAD + 1]), c * F + f)
         if c % 400 == 0 or c == CHUNKS - 1:
             check_state(cache, oc, where=c)
+            if update == "staged":
+                cache.verify()
             print(f"chunk {c}: state matches ({len(oc.merge_log)} consolidations, "
                   f"{oc.anchor_merges} anchor merges)", flush=True)
     st = cache.state()

@@ -78,3 +78,25 @@ def test_bf16_peaked_softmax():
 def test_bf16_wan_heads_small_tokens():
     # Wan-class head layout (12 x 128) with few tokens per frame.
     run_chunks(H=12, D=128, N=64, F=3, M=21, chunks=10, check_every_entry=False)
+
+
+@pytest.mark.parametrize("N", [200, 40])
+def test_lse_request_leaves_the_output_unchanged(N):
+    """The kernel variant that also returns the log-sum-exp keeps a second
+    sum of the unrounded weights; O must be the same bits either way."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    H, D, F, M = 2, 128, 3, 5
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=torch.bfloat16)
+    gen = NumpyWanStream(17, N, H, D)
+    for c in range(4):
+        frames = [gen.frame() for _ in range(F)]
+        K = np.concatenate([f[0] for f in frames])
+        V = np.concatenate([f[1] for f in frames])
+        q = gen.queries(F * N) * np.float32(4.0)
+        qd, kd, vd = (torch.from_numpy(np.ascontiguousarray(x)).to("cuda", torch.bfloat16) for x in (q, K, V))
+        lse = torch.empty((H, F * N), dtype=torch.float32, device="cuda")
+        with_lse = cache.attend(qd, kd, vd, lse=lse)
+        without = cache.attend(qd, kd, vd)
+        assert torch.equal(with_lse.view(torch.int16), without.view(torch.int16)), c
+        cache.update(kd, vd, c * F)

@@ -18,11 +18,12 @@ pytestmark = pytest.mark.gpu
 
 
 def run_fullsize(H, D, N, F, M, chunks, layers=1, heads=(0,), check_layers=(0,), attn_chunks=(), rows=64,
-                 seed=0):
+                 seed=0, update="single", attend_layers=None):
     import torch
     from paper_2606_10671_amd.fademem import Cache
     from paper_2606_10671_amd.synth import TorchWanStream
-    print(f"fullsize H={H} D={D} N={N} F={F} M={M} chunks={chunks} layers={layers} heads={heads}", flush=True)
+    print(f"fullsize H={H} D={D} N={N} F={F} M={M} chunks={chunks} layers={layers} heads={heads} update={update}",
+          flush=True)
     cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=torch.bfloat16,
                   layers=layers)
     streams = [TorchWanStream(seed + 1000 * l, N, H, D) for l in range(layers)]
@@ -33,7 +34,7 @@ def run_fullsize(H, D, N, F, M, chunks, layers=1, heads=(0,), check_layers=(0,),
     worst = [0.0, 0.0, 0.0]
     for c in range(chunks):
         data = [streams[l].chunk(F) for l in range(layers)]
-        for l in range(layers):
+        for l in range(layers) if attend_layers is None else attend_layers:
             q, k, v = data[l]
             cache.attend(q, k, v, layer=l, out=out, lse=lse)
             if c in attn_chunks and l in check_layers:
@@ -51,11 +52,14 @@ def run_fullsize(H, D, N, F, M, chunks, layers=1, heads=(0,), check_layers=(0,),
                     worst = [max(worst[0], err), max(worst[1], norm), max(worst[2], lerr)]
                     assert err <= BF16_MAX_ABS and norm <= BF16_NORM_RTOL and lerr <= BF16_LSE_ABS, (c, l, h, err,
                                                                                                    norm, lerr)
+        if update == "fused":
+            cache.update([data[l][1] for l in range(layers)], [data[l][2] for l in range(layers)], c * F)
         for f in range(F):
             ks = [data[l][1][f * N:(f + 1) * N] for l in range(layers)]
             vs = [data[l][2][f * N:(f + 1) * N] for l in range(layers)]
-            cache.insert(ks, vs, c * F + f)
-            cache.consolidate()
+            if update == "single":
+                cache.insert(ks, vs, c * F + f)
+                cache.consolidate()
             for (l, h), oc in ocs.items():
                 oc.update(to_np(ks[l][:, h:h + 1]), to_np(vs[l][:, h:h + 1]), c * F + f)
         check_state(cache, next(iter(ocs.values())), where=c)
@@ -91,3 +95,14 @@ def test_14b_class_layer():
     """14B-class layer at 720p: 40 heads x 128, 3600 tokens per frame
     (10 800 queries, 86 400 keys at steady state)."""
     run_fullsize(H=40, D=128, N=3600, F=3, M=21, chunks=9, heads=(0, 39), attn_chunks=(8,), rows=32)
+
+
+def test_14b_class_forty_layers_fused():
+    """The 14B-class configuration as benchmarked: 40 layers in one cache
+    (64.9 GB of K/V slots), 40 heads x 128, 3600 tokens per frame, fused
+    chunk updates.  Layers 0 and 39 are tracked bit for bit (one head
+    each) and attended on sampled rows at the last chunk, which sees the
+    full memory (86 400 keys)."""
+    run_fullsize(H=40, D=128, N=3600, F=3, M=21, chunks=9, layers=40, heads=(11,), check_layers=(0, 39),
+                 attn_chunks=(8,), rows=32, update="fused", attend_layers=(0, 39))
+

@@ -110,3 +110,82 @@ def test_rope_wan_shape():
                       c * F + f)
     check_state(cache, oc)
     check_entries(cache, oc, head_slice=slice(head, head + 1))
+
+
+def test_rope_attend_between_insert_and_consolidate():
+    """With M + 1 entries held (after an insert, before its consolidation)
+    the re-indexed view exposes all of them, entry M at index M."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    H, D, N, M, P, steps = 2, 128, 72, 4, 22, 12
+    print(f"rope insert-then-attend H={H} N={N} M={M} P={P} steps={steps}", flush=True)
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=torch.bfloat16,
+                  rope_pairs=P)
+    oc = OracleCache(budget=M, beta=0.3, anchor=True, storage="bf16")
+    gen = NumpyWanStream(5, N, H, D)
+    seen_full = False
+    for t in range(steps):
+        k, v = gen.frame()
+        kd, vd = (torch.from_numpy(np.ascontiguousarray(x)).to("cuda", torch.bfloat16) for x in (k, v))
+        cache.insert(kd, vd, t)
+        oc.insert(k, v, t)
+        n = len(oc.entries)
+        seen_full = seen_full or n == M + 1
+        q = gen.queries(N)
+        qr = rope_rotate(q, n, P, 10000.0, "bf16")       # the caller's chunk at index n
+        kc, vc = gen.frame()
+        kcr = rope_rotate(kc, n, P, 10000.0, "bf16")
+        qd, kcd, vcd = (torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to("cuda", torch.bfloat16)
+                        for x in (qr, kcr, vc))
+        lse = torch.empty((H, N), dtype=torch.float32, device="cuda")
+        out = cache.attend(qd, kcd, vcd, lse=lse)
+        Km, Vm = exposed_kv_rope(oc, P, 10000.0)
+        O_ref, L_ref = attend(qr, Km, Vm, kcr, vc)
+        check_attention(to_np(out), to_np(lse), O_ref, L_ref, "bf16", where=("held", n))
+        cache.consolidate()
+        oc.consolidate()
+        cache.verify()
+        check_state(cache, oc, where=t)
+    assert seen_full
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_rope_views_per_layer_across_denoising_steps(dtype):
+    """Several layers, each attended several times per chunk (one call per
+    denoising step) before the update: every call must see its own layer's
+    memory re-indexed, whichever layer was attended last."""
+    import torch
+    from paper_2606_10671_amd.fademem import Cache
+    H, D, N, F, M, P, L, chunks, steps = 2, 64, 40, 2, 4, 11, 3, 7, 3
+    print(f"rope layers={L} steps={steps} dtype={dtype}", flush=True)
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=0.3, anchor=True, dtype=td, layers=L,
+                  rope_pairs=P)
+    ocs = [OracleCache(budget=M, beta=0.3, anchor=True, storage=dtype) for _ in range(L)]
+    gens = [NumpyWanStream(40 + l, N, H, D) for l in range(L)]
+    for c in range(chunks):
+        frames = [[g.frame() for _ in range(F)] for g in gens]
+        Ks = [np.concatenate([f[0] for f in fr]) for fr in frames]
+        Vs = [np.concatenate([f[1] for f in fr]) for fr in frames]
+        n = len(ocs[0].entries)
+        for s in range(steps):
+            for l in (range(L) if s % 2 == 0 else reversed(range(L))):
+                q = gens[l].queries(F * N)
+                qr = np.concatenate([rope_rotate(q[f * N:(f + 1) * N], n + f, P, 10000.0, dtype) for f in range(F)])
+                kr = np.concatenate([rope_rotate(Ks[l][f * N:(f + 1) * N], n + f, P, 10000.0, dtype)
+                                     for f in range(F)])
+                qd, krd, vd = (torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to("cuda", td)
+                               for x in (qr, kr, Vs[l]))
+                lse = torch.empty((H, F * N), dtype=torch.float32, device="cuda")
+                out = cache.attend(qd, krd, vd, layer=l, lse=lse)
+                Km, Vm = exposed_kv_rope(ocs[l], P, 10000.0)
+                O_ref, L_ref = attend(qr, Km, Vm, kr, Vs[l])
+                check_attention(to_np(out), to_np(lse), O_ref, L_ref, dtype, where=(c, s, l))
+        kd = [torch.from_numpy(np.ascontiguousarray(x)).to("cuda", td) for x in Ks]
+        vd = [torch.from_numpy(np.ascontiguousarray(x)).to("cuda", td) for x in Vs]
+        cache.update(kd, vd, c * F)
+        for l in range(L):
+            for f in range(F):
+                ocs[l].update(frames[l][f][0], frames[l][f][1], c * F + f)
+        check_state(cache, ocs[0], where=c)
+    cache.verify()
