@@ -578,42 +578,13 @@ struct UpdateDataArgs {
   int64_t units;   // 16-byte units per K (or V) block
 };
 
+// grid.y = layer * 2 + kv: the blocks of a (layer, K|V) plane stride over
+// it, every plane of the launch streamed at once.
 template <bool BF16, bool MAXOP>
 __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
   constexpr int kM = kMaxPlanFrames, kO = 2 * kMaxPlanFrames;
   const UpdatePlan* P = reinterpret_cast<const UpdatePlan*>(a.pool + a.lay.off_prog);
   const int n_ar = P->n_ar, n_out = P->n_out;
-  const int li = blockIdx.y >> 1, kv = blockIdx.y & 1;
-  const int64_t layer = a.layer0 + li;
-  const char* chunk = static_cast<const char*>(kv ? a.v[li] : a.k[li]);
-  auto ref = [&](int kind, int idx) -> const u32x4* {
-    return reinterpret_cast<const u32x4*>(kind == kRefSlot ? a.pool + kv_offset(a.lay, layer, idx, kv)
-                                                           : chunk + size_t(idx) * a.lay.blk_bytes);
-  };
-  const u32x4* pa[kM];
-  const u32x4* pb[kM];
-  int ra[kM], rb[kM];
-  double wa[kM], wb[kM];
-#pragma unroll
-  for (int k = 0; k < kM; ++k) {
-    const bool on = k < n_ar;
-    ra[k] = on && P->a_kind[k] == kRefResult ? P->a_idx[k] : -1;
-    rb[k] = on && P->b_kind[k] == kRefResult ? P->b_idx[k] : -1;
-    pa[k] = on && ra[k] < 0 ? ref(P->a_kind[k], P->a_idx[k]) : nullptr;
-    pb[k] = on && rb[k] < 0 ? ref(P->b_kind[k], P->b_idx[k]) : nullptr;
-    wa[k] = on ? P->wa[k] : 0.0;
-    wb[k] = on ? P->wb[k] : 0.0;
-  }
-  u32x4* po[kO];
-  const u32x4* ps[kO];
-  int ro[kO];
-#pragma unroll
-  for (int o = 0; o < kO; ++o) {
-    const bool on = o < n_out;
-    ro[o] = on && P->o_kind[o] == kRefResult ? P->o_idx[o] : -1;
-    ps[o] = on && ro[o] < 0 ? ref(P->o_kind[o], P->o_idx[o]) : nullptr;
-    po[o] = on ? reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, layer, P->o_slot[o], kv)) : nullptr;
-  }
   // Result r of the merges computed so far (r is wave-uniform).
   auto pick = [](const u32x4 (&R)[kM], int r) {
     u32x4 x = R[0];
@@ -622,31 +593,64 @@ __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
       if (r == k) x = R[k];
     return x;
   };
-  const int64_t stride = int64_t(gridDim.x) * 256;
-  for (int64_t u = int64_t(blockIdx.x) * 256 + threadIdx.x; u < a.units; u += stride) {
-    // Every operand of this unit is loaded before any store (stores may go
-    // to a slot an operand was read from).
-    u32x4 A[kM], B[kM], S[kO], R[kM];
+  auto run_plane = [&](int li, int kv, int64_t u_begin, int64_t u_end, int64_t u_step) {
+    const int64_t layer = a.layer0 + li;
+    const char* chunk = static_cast<const char*>(kv ? a.v[li] : a.k[li]);
+    auto ref = [&](int kind, int idx) -> const u32x4* {
+      return reinterpret_cast<const u32x4*>(kind == kRefSlot ? a.pool + kv_offset(a.lay, layer, idx, kv)
+                                                             : chunk + size_t(idx) * a.lay.blk_bytes);
+    };
+    const u32x4* pa[kM];
+    const u32x4* pb[kM];
+    int ra[kM], rb[kM];
+    double wa[kM], wb[kM];
 #pragma unroll
     for (int k = 0; k < kM; ++k) {
-      if (pa[k]) A[k] = __builtin_nontemporal_load(pa[k] + u);
-      if (pb[k]) B[k] = __builtin_nontemporal_load(pb[k] + u);
+      const bool on = k < n_ar;
+      ra[k] = on && P->a_kind[k] == kRefResult ? P->a_idx[k] : -1;
+      rb[k] = on && P->b_kind[k] == kRefResult ? P->b_idx[k] : -1;
+      pa[k] = on && ra[k] < 0 ? ref(P->a_kind[k], P->a_idx[k]) : nullptr;
+      pb[k] = on && rb[k] < 0 ? ref(P->b_kind[k], P->b_idx[k]) : nullptr;
+      wa[k] = on ? P->wa[k] : 0.0;
+      wb[k] = on ? P->wb[k] : 0.0;
     }
+    u32x4* po[kO];
+    const u32x4* ps[kO];
+    int ro[kO];
 #pragma unroll
-    for (int o = 0; o < kO; ++o)
-      if (ps[o]) S[o] = __builtin_nontemporal_load(ps[o] + u);
+    for (int o = 0; o < kO; ++o) {
+      const bool on = o < n_out;
+      ro[o] = on && P->o_kind[o] == kRefResult ? P->o_idx[o] : -1;
+      ps[o] = on && ro[o] < 0 ? ref(P->o_kind[o], P->o_idx[o]) : nullptr;
+      po[o] = on ? reinterpret_cast<u32x4*>(a.pool + kv_offset(a.lay, layer, P->o_slot[o], kv)) : nullptr;
+    }
+    for (int64_t u = u_begin; u < u_end; u += u_step) {
+      // Every operand of this unit is loaded before any store (stores may go
+      // to a slot an operand was read from).
+      u32x4 A[kM], B[kM], S[kO], R[kM];
 #pragma unroll
-    for (int k = 0; k < kM; ++k) {
-      if (k < n_ar) {
-        const u32x4 x = pa[k] ? A[k] : pick(R, ra[k]);
-        const u32x4 y = pb[k] ? B[k] : pick(R, rb[k]);
-        R[k] = merge_unit<BF16, MAXOP>(x, y, wa[k], wb[k]);
+      for (int k = 0; k < kM; ++k) {
+        if (pa[k]) A[k] = __builtin_nontemporal_load(pa[k] + u);
+        if (pb[k]) B[k] = __builtin_nontemporal_load(pb[k] + u);
       }
-    }
 #pragma unroll
-    for (int o = 0; o < kO; ++o)
-      if (po[o]) __builtin_nontemporal_store(ps[o] ? S[o] : pick(R, ro[o]), po[o] + u);
-  }
+      for (int o = 0; o < kO; ++o)
+        if (ps[o]) S[o] = __builtin_nontemporal_load(ps[o] + u);
+#pragma unroll
+      for (int k = 0; k < kM; ++k) {
+        if (k < n_ar) {
+          const u32x4 x = pa[k] ? A[k] : pick(R, ra[k]);
+          const u32x4 y = pb[k] ? B[k] : pick(R, rb[k]);
+          R[k] = merge_unit<BF16, MAXOP>(x, y, wa[k], wb[k]);
+        }
+      }
+#pragma unroll
+      for (int o = 0; o < kO; ++o)
+        if (po[o]) __builtin_nontemporal_store(ps[o] ? S[o] : pick(R, ro[o]), po[o] + u);
+    }
+  };
+  run_plane(blockIdx.y >> 1, blockIdx.y & 1, int64_t(blockIdx.x) * 256 + threadIdx.x, a.units,
+            int64_t(gridDim.x) * 256);
 }
 
 // ---------------------------------------------------------------------------
@@ -1110,6 +1114,7 @@ int fademem_consolidate(fademem_cache* c, void* stream) {
   const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
   auto kernel = bf16 ? (maxop ? consolidate_kernel<true, kMergeUnroll, true> : consolidate_kernel<true, kMergeUnroll, false>)
                      : (maxop ? consolidate_kernel<false, kMergeUnroll, true> : consolidate_kernel<false, kMergeUnroll, false>);
+
   // One resident round of blocks over the planes (every block also derives
   // the schedule, so no more blocks than the device holds at once).
   const unsigned planes = unsigned(2 * c->cfg.layers);
@@ -1163,10 +1168,10 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
   }
   (void)hipGetLastError();
   const int64_t units = int64_t(c->lay.blk_bytes / 16);
-  const unsigned planes_max = unsigned(2 * (layers < kMaxLayersPerLaunch ? layers : kMaxLayersPerLaunch));
   const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
   auto data_kernel = bf16 ? (maxop ? update_data_kernel<true, true> : update_data_kernel<true, false>)
                           : (maxop ? update_data_kernel<false, true> : update_data_kernel<false, false>);
+  const unsigned planes_max = unsigned(2 * (layers < kMaxLayersPerLaunch ? layers : kMaxLayersPerLaunch));
   const unsigned per_plane = stream_blocks_per_plane(reinterpret_cast<const void*>(data_kernel), planes_max, units, 1);
   for (int64_t f0 = 0; f0 < frames; f0 += kMaxPlanFrames) {
     const int nf = int((frames - f0) < kMaxPlanFrames ? (frames - f0) : kMaxPlanFrames);
