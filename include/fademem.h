@@ -306,6 +306,37 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
  * Errors: EINVAL (NULL cache), EHIP. */
 int fademem_verify(fademem_cache* cache, void* stream);
 
+/* Host steps of the spectral-decay analysis (Sec. 3.2; supplementary Sec.
+ * S2) on small host arrays; they read and write host memory only, enqueue
+ * nothing and need no device.  The paper gives the radial frequency, the
+ * horizon as the onset of the near-flat regime after the main decay, and a
+ * nonlinear least-squares fit of r*(t) = a t^(-b); the band edges, the
+ * smoothing and the threshold are this library's readings.
+ *
+ * fademem_spectral_band_map: band_of (host int32 [height][width]) receives
+ * the band of DCT coefficient (u, v): `bands` equal-width bins of
+ * r = sqrt((u/H)^2 + (v/W)^2) over [0, max r], the last bin closed, the DC
+ * coefficient -1 (left out); centres (host double [bands], may be NULL)
+ * the bins' centre radii.  1 <= height, width <= 1024, 1 <= bands <= 1024.
+ *
+ * fademem_spectral_horizons: corr (host double [bands][lags], row k = band
+ * k's C_k(lag)); each row is smoothed by a centred moving average over
+ * `window` lags (shrinking at the ends); horizon[k] (host int64 [bands]) is
+ * the first lag >= 1 at which the smoothed curve has made at least half of
+ * its total decay and falls to the next lag by less than `drop` times its
+ * steepest one-lag fall, or -1 (the defaults used here: window 5, drop 0.05).
+ *
+ * fademem_spectral_fit: (a, b) of r = a t^(-b) minimising sum (r_i - a
+ * t_i^(-b))^2 over n >= 2 points with t_i, r_i > 0: Gauss-Newton from the
+ * straight-line fit of log r on log t, at most `iters` steps.
+ *
+ * Errors: EINVAL (NULL pointers, sizes out of range, non-positive or
+ * infinite points, a fit that does not converge to finite values), ENOMEM. */
+int fademem_spectral_band_map(int32_t height, int32_t width, int32_t bands, int32_t* band_of, double* centres);
+int fademem_spectral_horizons(const double* corr, int32_t bands, int64_t lags, int32_t window, double drop,
+                              int64_t* horizon);
+int fademem_spectral_fit(const double* t, const double* r, int64_t n, int32_t iters, double* a, double* b);
+
 /* hipError_t value of the last FADEMEM_EHIP on this cache (0 if none). */
 int fademem_last_hip_error(const fademem_cache* cache);
 

@@ -36,6 +36,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <vector>
+
 #include "fademem_internal.h"
 
 namespace {
@@ -739,6 +741,128 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
   hipLaunchKernelGGL(clip_mean_kernel, dim3(unsigned((outs + kMeanOuts - 1) / kMeanOuts)),
                      dim3(kMeanOuts * kMeanGroups), 0, s, per_clip, start, clips, nlag, int(bands), corr);
   return hipGetLastError() == hipSuccess ? FADEMEM_OK : FADEMEM_EHIP;
+}
+
+
+// ---------------------------------------------------------------------------
+// Host steps of the analysis (Sec. 3.2, supplementary Sec. S2) on the
+// correlation curves: a few dozen numbers, no device work.
+// ---------------------------------------------------------------------------
+
+// Radial bands: bands equal-width bins of r(u, v) = sqrt((u/H)^2 + (v/W)^2)
+// over [0, max r], the last bin closed, the DC coefficient left out (-1);
+// a band's radius is its bin centre.
+int fademem_spectral_band_map(int32_t height, int32_t width, int32_t bands, int32_t* band_of, double* centres) {
+  if (!band_of || height < 1 || width < 1 || height > 1024 || width > 1024 || bands < 1 || bands > kSpecMaxBands)
+    return FADEMEM_EINVAL;
+  auto radius = [&](int u, int v) {
+    const double a = double(u) / double(height), b = double(v) / double(width);
+    return sqrt(a * a + b * b);
+  };
+  const double r_max = radius(height - 1, width - 1);
+  for (int u = 0; u < height; ++u)
+    for (int v = 0; v < width; ++v) {
+      int32_t k = -1;
+      if (u != 0 || v != 0) {
+        const double x = floor(radius(u, v) / r_max * double(bands));
+        k = x >= double(bands - 1) ? bands - 1 : int32_t(x);
+      }
+      band_of[size_t(u) * size_t(width) + size_t(v)] = k;
+    }
+  if (centres)
+    for (int k = 0; k < bands; ++k) centres[k] = (double(k) + 0.5) * r_max / double(bands);
+  return FADEMEM_OK;
+}
+
+// Decorrelation horizon of each band's curve corr[k][0..lags-1]: smooth it
+// with a centred moving average over `window` lags (shrinking at the ends);
+// the horizon is the first lag >= 1, once the smoothed curve has made at
+// least half of its total decay (s[0] - min s), where its next one-lag fall
+// is below `drop` times its steepest one-lag fall; -1 if there is none (or
+// the curve never falls).
+int fademem_spectral_horizons(const double* corr, int32_t bands, int64_t lags, int32_t window, double drop,
+                              int64_t* horizon) {
+  if (!corr || !horizon || bands < 1 || lags < 1 || lags > (int64_t(1) << 24) || window < 1 || !(drop >= 0.0))
+    return FADEMEM_EINVAL;
+  std::vector<double> sm;
+  try {
+    sm.resize(size_t(lags));
+  } catch (...) {
+    return FADEMEM_ENOMEM;
+  }
+  const int64_t h = window / 2;
+  for (int k = 0; k < bands; ++k) {
+    const double* c = corr + size_t(k) * size_t(lags);
+    for (int64_t i = 0; i < lags; ++i) {
+      const int64_t lo = i - h < 0 ? 0 : i - h, hi = i + h + 1 < lags ? i + h + 1 : lags;
+      double sum = 0.0;
+      for (int64_t j = lo; j < hi; ++j) sum += c[j];
+      sm[size_t(i)] = sum / double(hi - lo);
+    }
+    double lowest = sm[0], steepest = -INFINITY;
+    for (int64_t i = 0; i < lags; ++i) lowest = fmin(lowest, sm[size_t(i)]);
+    for (int64_t i = 0; i + 1 < lags; ++i) steepest = fmax(steepest, sm[size_t(i)] - sm[size_t(i) + 1]);
+    const double total = sm[0] - lowest;
+    horizon[k] = -1;
+    if (!(total > 0.0 && steepest > 0.0)) continue;
+    for (int64_t lag = 1; lag + 1 < lags; ++lag) {
+      if (sm[0] - sm[size_t(lag)] >= 0.5 * total && sm[size_t(lag)] - sm[size_t(lag) + 1] < drop * steepest) {
+        horizon[k] = lag;
+        break;
+      }
+    }
+  }
+  return FADEMEM_OK;
+}
+
+// r = a t^(-b) fitted to n points by least squares on r: Gauss-Newton on
+// the residuals r_i - a t_i^(-b), started from the straight line through
+// (log t, log r); stops when a step changes a and b by less than 1e-14
+// relative, or after `iters` steps.
+int fademem_spectral_fit(const double* t, const double* r, int64_t n, int32_t iters, double* a_out, double* b_out) {
+  if (!t || !r || !a_out || !b_out || n < 2 || iters < 0) return FADEMEM_EINVAL;
+  for (int64_t i = 0; i < n; ++i)
+    if (!(t[i] > 0.0) || !(r[i] > 0.0) || isinf(t[i]) || isinf(r[i])) return FADEMEM_EINVAL;
+  double mx = 0.0, my = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    mx += log(t[i]);
+    my += log(r[i]);
+  }
+  mx /= double(n);
+  my /= double(n);
+  double sxx = 0.0, sxy = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    const double dx = log(t[i]) - mx, dy = log(r[i]) - my;
+    sxx += dx * dx;
+    sxy += dx * dy;
+  }
+  if (!(sxx > 0.0)) return FADEMEM_EINVAL;  // every t equal: the exponent is not determined
+  const double slope = sxy / sxx;
+  double a = exp(my - slope * mx), b = -slope;
+  for (int it = 0; it < iters; ++it) {
+    // Normal equations of the linearised problem: J = [df/da, df/db].
+    double jaa = 0.0, jab = 0.0, jbb = 0.0, ga = 0.0, gb = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+      const double lt = log(t[i]);
+      const double f = a * exp(-b * lt);
+      const double da = f / a, db = -lt * f, res = r[i] - f;
+      jaa += da * da;
+      jab += da * db;
+      jbb += db * db;
+      ga += da * res;
+      gb += db * res;
+    }
+    const double det = jaa * jbb - jab * jab;
+    if (!(det != 0.0) || isinf(det)) break;
+    const double sa = (jbb * ga - jab * gb) / det, sb = (jaa * gb - jab * ga) / det;
+    a += sa;
+    b += sb;
+    if (fabs(sa) <= 1e-14 * fmax(1.0, fabs(a)) && fabs(sb) <= 1e-14 * fmax(1.0, fabs(b))) break;
+  }
+  if (!isfinite(a) || !isfinite(b)) return FADEMEM_EINVAL;
+  *a_out = a;
+  *b_out = b;
+  return FADEMEM_OK;
 }
 
 }  // extern "C"

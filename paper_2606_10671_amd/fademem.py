@@ -35,7 +35,8 @@ EXPORTED = (
     "fademem_consolidate", "fademem_update", "fademem_attend", "fademem_count", "fademem_get_state",
     "fademem_entry_kv", "fademem_set_state", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
     "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr", "fademem_stage",
-    "fademem_update_staged", "fademem_attend_staged", "fademem_verify",
+    "fademem_update_staged", "fademem_attend_staged", "fademem_verify", "fademem_spectral_band_map",
+    "fademem_spectral_horizons", "fademem_spectral_fit",
 )
 
 
@@ -117,6 +118,10 @@ def lib() -> ctypes.CDLL:
     L.fademem_attend_staged.argtypes = [c_void_p, c_int32, c_void_p, c_int64, c_int64, ctypes.c_float, c_void_p,
                                         c_void_p, c_void_p]
     L.fademem_verify.argtypes = [c_void_p, c_void_p]
+    L.fademem_spectral_band_map.argtypes = [c_int32, c_int32, c_int32, c_void_p, c_void_p]
+    L.fademem_spectral_horizons.argtypes = [c_void_p, c_int32, c_int64, c_int32, ctypes.c_double, c_void_p]
+    L.fademem_spectral_fit.argtypes = [c_void_p, c_void_p, c_int64, c_int32, P(ctypes.c_double),
+                                       P(ctypes.c_double)]
     L.fademem_last_hip_error.argtypes = [c_void_p]
     for name in EXPORTED:
         if name != "fademem_strerror":
@@ -277,6 +282,24 @@ def fademem_spectral_corr(latents_ptr: int, clips: int, frames: int, height: int
                                     ctypes.c_void_p(band_of_ptr), bands, max_lag, ctypes.c_void_p(workspace_ptr),
                                     workspace_bytes, ctypes.c_void_p(corr_ptr), ctypes.c_void_p(stream)),
         "fademem_spectral_corr")
+
+
+def fademem_spectral_band_map(height: int, width: int, bands: int, band_of_ptr: int, centres_ptr: int = 0) -> None:
+    _ok(lib().fademem_spectral_band_map(height, width, bands, ctypes.c_void_p(band_of_ptr),
+                                        ctypes.c_void_p(centres_ptr)), "fademem_spectral_band_map")
+
+
+def fademem_spectral_horizons(corr_ptr: int, bands: int, lags: int, window: int, drop: float,
+                              horizon_ptr: int) -> None:
+    _ok(lib().fademem_spectral_horizons(ctypes.c_void_p(corr_ptr), bands, lags, window, drop,
+                                        ctypes.c_void_p(horizon_ptr)), "fademem_spectral_horizons")
+
+
+def fademem_spectral_fit(t_ptr: int, r_ptr: int, n: int, iters: int = 100):
+    a, b = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _ok(lib().fademem_spectral_fit(ctypes.c_void_p(t_ptr), ctypes.c_void_p(r_ptr), n, iters, ctypes.byref(a),
+                                   ctypes.byref(b)), "fademem_spectral_fit")
+    return a.value, b.value
 
 
 def fademem_last_hip_error(handle: int) -> int:
