@@ -59,8 +59,10 @@ enum {
   FADEMEM_ENOMEM = -3,     /* caller's pool smaller than fademem_pool_bytes      */
   FADEMEM_EHIP = -4,       /* HIP runtime or launch error                        */
   FADEMEM_EUNSUPPORTED = -5,/* valid request this build does not implement       */
-  FADEMEM_EINTERNAL = -6   /* host replay of the memory state disagrees with the
+  FADEMEM_EINTERNAL = -6,  /* host replay of the memory state disagrees with the
                               device (fademem_verify, serialize mode)           */
+  FADEMEM_ESCRATCH = -7    /* request larger than the static scratch of an
+                              allocation-free entry point                       */
 };
 
 enum { FADEMEM_F32 = 0, FADEMEM_BF16 = 1 };
@@ -305,6 +307,21 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
  * EINTERNAL (serialize mode runs the same check after every call).
  * Errors: EINVAL (NULL cache), EHIP. */
 int fademem_verify(fademem_cache* cache, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * analysis as fademem_spectral_corr, with its workspace in a static scratch
+ * array of the library (64 MiB per GPU, held by each GPU the library runs on
+ * until the process ends) instead of a caller's buffer; the caller still
+ * passes the inputs and corr.  The call allocates nothing.  Requests whose
+ * workspace (fademem_spectral_workspace_bytes) exceeds 64 MiB return
+ * FADEMEM_ESCRATCH before anything is enqueued (the 374-clip analysis of
+ * supplementary Sec. S2 needs 38.2 MB).  All calls on one GPU share its
+ * scratch: calls that overlap on one GPU (several streams or threads) race.
+ * Errors: as fademem_spectral_corr, plus ESCRATCH. */
+int fademem_spectral_corr_static(const float* latents, int64_t clips, int64_t frames, int32_t height,
+                                 int32_t width, const int32_t* band_of, int32_t bands, int64_t max_lag,
+                                 double* corr, void* stream);
 
 /* Host steps of the spectral-decay analysis (Sec. 3.2; supplementary Sec.
  * S2) on small host arrays; they read and write host memory only, enqueue

@@ -982,6 +982,7 @@ const char* fademem_strerror(int code) {
     case FADEMEM_EHIP: return "HIP runtime or launch error";
     case FADEMEM_EUNSUPPORTED: return "not supported by this build";
     case FADEMEM_EINTERNAL: return "host replay of the memory state disagrees with the device";
+    case FADEMEM_ESCRATCH: return "request exceeds the static scratch of the allocation-free entry point";
     default: return "unknown error";
   }
 }

@@ -36,6 +36,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "fademem_internal.h"
@@ -672,6 +673,38 @@ bool is_aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p
 
 }  // namespace
 
+// Workspace of the allocation-free entry point: one copy per GPU, in the
+// library's code object, held until the process ends.  Host code never
+// passes this name to a kernel (on the host it is only a stand-in for the
+// symbol): it uses the device address hipGetSymbolAddress returns for the
+// current device.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices];  // device address of `scratch` per device, once looked up
+
+// The current device's copy of `scratch` (looked up on the first call on
+// that device, with it current).
+int static_scratch(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FADEMEM_EHIP;
+  if (dev < 0 || dev >= kMaxScratchDevices) return FADEMEM_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FADEMEM_EHIP;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return FADEMEM_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int fademem_spectral_workspace_bytes(int64_t clips, int64_t frames, int32_t height, int32_t width, int32_t bands,
@@ -743,6 +776,28 @@ int fademem_spectral_corr(const float* latents, int64_t clips, int64_t frames, i
   return hipGetLastError() == hipSuccess ? FADEMEM_OK : FADEMEM_EHIP;
 }
 
+
+// The same analysis with its workspace in the library's static scratch of
+// the current device: no allocation, no workspace argument.  Requests whose
+// workspace would exceed kStaticScratchBytes are refused before anything is
+// enqueued.  Every call on a GPU shares that GPU's scratch: calls that
+// overlap on one GPU (other streams, other threads) race.  The kernels write
+// every scratch byte they read, so nothing needs clearing between calls.
+int fademem_spectral_corr_static(const float* latents, int64_t clips, int64_t frames, int32_t height, int32_t width,
+                                 const int32_t* band_of, int32_t bands, int64_t max_lag, double* corr,
+                                 void* stream) {
+  if (!latents || !band_of || !corr) return FADEMEM_EINVAL;
+  if (!spec_args_ok(clips, frames, height, width, bands, max_lag)) return FADEMEM_EINVAL;
+  SpecLayout L;
+  if (!spec_layout(clips, max_lag + 1, height, width, bands, fused_fits(height, width, bands), &L))
+    return FADEMEM_EINVAL;
+  if (L.total > kStaticScratchBytes) return FADEMEM_ESCRATCH;
+  void* ws = nullptr;
+  const int rc = static_scratch(&ws);
+  if (rc != FADEMEM_OK) return rc;
+  return fademem_spectral_corr(latents, clips, frames, height, width, band_of, bands, max_lag, ws,
+                               kStaticScratchBytes, corr, stream);
+}
 
 // ---------------------------------------------------------------------------
 // Host steps of the analysis (Sec. 3.2, supplementary Sec. S2) on the

@@ -21,6 +21,7 @@ FADEMEM_ENOMEM = -3
 FADEMEM_EHIP = -4
 FADEMEM_EUNSUPPORTED = -5
 FADEMEM_EINTERNAL = -6
+FADEMEM_ESCRATCH = -7
 FADEMEM_F32 = 0
 FADEMEM_BF16 = 1
 FADEMEM_MERGE_SQRT_SPAN = 0
@@ -36,7 +37,7 @@ EXPORTED = (
     "fademem_entry_kv", "fademem_set_state", "fademem_merge_log", "fademem_merge_counts", "fademem_last_hip_error",
     "fademem_strerror", "fademem_spectral_workspace_bytes", "fademem_spectral_corr", "fademem_stage",
     "fademem_update_staged", "fademem_attend_staged", "fademem_verify", "fademem_spectral_band_map",
-    "fademem_spectral_horizons", "fademem_spectral_fit",
+    "fademem_spectral_horizons", "fademem_spectral_fit", "fademem_spectral_corr_static",
 )
 
 
@@ -118,6 +119,8 @@ def lib() -> ctypes.CDLL:
     L.fademem_attend_staged.argtypes = [c_void_p, c_int32, c_void_p, c_int64, c_int64, ctypes.c_float, c_void_p,
                                         c_void_p, c_void_p]
     L.fademem_verify.argtypes = [c_void_p, c_void_p]
+    L.fademem_spectral_corr_static.argtypes = [c_void_p, c_int64, c_int64, c_int32, c_int32, c_void_p, c_int32,
+                                               c_int64, c_void_p, c_void_p]
     L.fademem_spectral_band_map.argtypes = [c_int32, c_int32, c_int32, c_void_p, c_void_p]
     L.fademem_spectral_horizons.argtypes = [c_void_p, c_int32, c_int64, c_int32, ctypes.c_double, c_void_p]
     L.fademem_spectral_fit.argtypes = [c_void_p, c_void_p, c_int64, c_int32, P(ctypes.c_double),
@@ -282,6 +285,13 @@ def fademem_spectral_corr(latents_ptr: int, clips: int, frames: int, height: int
                                     ctypes.c_void_p(band_of_ptr), bands, max_lag, ctypes.c_void_p(workspace_ptr),
                                     workspace_bytes, ctypes.c_void_p(corr_ptr), ctypes.c_void_p(stream)),
         "fademem_spectral_corr")
+
+
+def fademem_spectral_corr_static(latents_ptr: int, clips: int, frames: int, height: int, width: int,
+                                 band_of_ptr: int, bands: int, max_lag: int, corr_ptr: int, stream: int = 0) -> None:
+    _ok(lib().fademem_spectral_corr_static(ctypes.c_void_p(latents_ptr), clips, frames, height, width,
+                                           ctypes.c_void_p(band_of_ptr), bands, max_lag, ctypes.c_void_p(corr_ptr),
+                                           ctypes.c_void_p(stream)), "fademem_spectral_corr_static")
 
 
 def fademem_spectral_band_map(height: int, width: int, bands: int, band_of_ptr: int, centres_ptr: int = 0) -> None:

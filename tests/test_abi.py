@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_strerror_covers_all_codes():
     for code in (fm.FADEMEM_OK, fm.FADEMEM_EINVAL, fm.FADEMEM_ESTATE, fm.FADEMEM_ENOMEM, fm.FADEMEM_EHIP,
-                 fm.FADEMEM_EUNSUPPORTED, fm.FADEMEM_EINTERNAL):
+                 fm.FADEMEM_EUNSUPPORTED, fm.FADEMEM_EINTERNAL, fm.FADEMEM_ESCRATCH):
         assert fm.fademem_strerror(code) != "unknown error"
     assert fm.fademem_strerror(-99) == "unknown error"
 
