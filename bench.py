@@ -53,14 +53,14 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 # split tiles) at the wan1.3b-1layer workload, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE (see profiles/attend_bf16_wan1.3b_1layer.md), valid only for the
 # kernel source they were taken on (first 16 hex digits of its sha256).
-ATTN_TRAFFIC = {"source_sha256": "ec7c162d9e33a366", "workload": "wan1.3b-1layer", "bytes_per_call": 760797874}
+ATTN_TRAFFIC = {"source_sha256": "7286bd87b8468878", "workload": "wan1.3b-1layer", "bytes_per_call": 761847800}
 
 
 # HBM bytes of one fused chunk update's data pass (update_data_kernel) in
 # the 30-layer update leg, from rocprofv3 FETCH_SIZE and WRITE_SIZE scaled
-# by the insert copy (see profiles/update_fused_wan1.3b_30layer.md); valid
+# by the insert copy (see profiles/update_data_wan1.3b_30layer.md); valid
 # only for the cache.hip source they were taken on.
-UPD_TRAFFIC = {"source_sha256": None, "workload": "wan1.3b-30layer-update", "bytes_per_call": None}
+UPD_TRAFFIC = {"source_sha256": "5e2914888716b334", "workload": "wan1.3b-30layer-update", "bytes_per_call": 4313367840}
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.
