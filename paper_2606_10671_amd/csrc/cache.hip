@@ -44,12 +44,15 @@ struct fademem_cache {
   bool serialize;       // FADEMEM_SERIALIZE set at creation: every call waits for its work and checks it
   int last_hip_error;
   Mirror mirror;
-  // Re-indexed K views (rope_pairs > 0): view position i of layer l holds
-  // the rotated K of the entry covering [view_first, view_first + view_span)
-  // (span 0: nothing valid).  An entry's covered range fixes its contents
-  // for the life of a cache: positions strictly increase and ranges only
-  // grow by merging.
+  // Re-indexed K views (rope_pairs > 0): view block s of layer l holds the
+  // K of slot s with its temporal pairs rotated to index view_index, built
+  // when the slot held the entry covering [view_first, view_first +
+  // view_span) (span 0: nothing valid).  An entry's covered range fixes its
+  // contents for the life of a cache: positions strictly increase and ranges
+  // only grow by merging.  An entry that only moved to another index (a
+  // merge before it) needs its temporal pairs rotated again, nothing else.
   std::vector<int64_t> view_first, view_span;
+  std::vector<int32_t> view_index;
 };
 
 namespace {
@@ -656,38 +659,42 @@ __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
 // ---------------------------------------------------------------------------
 // Temporal RoPE view (Sec. 3.3 "Boundary and positional handling"): memory
 // keys are stored without their temporal phase; for attention, entry e is
-// exposed at temporal index e.  This kernel writes entry e's K with pairs
-// k < P rotated by the angle e * w_k, w_k = theta^(-k/P) (fp64, rounded once
-// to the storage type), into K block e of the layer's view; V is read from
-// the entry's slot as stored.  Only the listed view positions are written
-// (those whose entry changed since the view was last built).
-// grid = (blocks per block, listed positions).
+// exposed at temporal index e.  The layer's view keeps one K block per slot:
+// this kernel writes slot s's K with pairs k < P rotated by the angle e * w_k,
+// w_k = theta^(-k/P) (fp64, rounded once to the storage type), e being the
+// index of the entry the slot holds, into view block s.  Attention reads K
+// through the slot table from the view and V from the slots.  Only listed
+// slots are written: in full when the slot's entry changed, or only the
+// 16-byte units holding temporal pairs when the entry just moved to another
+// index.  grid = (blocks per listed slot, listed slots).
 // ---------------------------------------------------------------------------
 
-constexpr int kMaxViewPos = 64;  // positions per launch
+constexpr int kMaxViewPos = 64;  // listed slots per launch
 
 struct RopeViewArgs {
   const char* kv_layer_base;  // pool + kv_offset(layer, 0, 0)
-  const int32_t* order;       // logical -> slot
-  char* view;                 // the layer's view: K block e at view + e * blk_stride
+  char* view;                 // the layer's view: K block s at view + s * blk_stride
   size_t slot_stride;         // 2 * blk_stride
   size_t blk_stride;
-  int64_t units;              // 16-byte units per K block
+  int64_t rows;               // N
+  int heads;
   int head_dim;
   int pairs;                  // P
   double theta;
   int n_pos;
-  int32_t pos[kMaxViewPos];   // view positions (= logical entries) to write
+  int32_t index[kMaxViewPos];  // temporal index of the entry
+  int32_t slot[kMaxViewPos];   // its slot
+  int32_t full[kMaxViewPos];   // 1: every unit; 0: the units holding temporal pairs
 };
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void rope_view_kernel(RopeViewArgs a) {
 #pragma clang fp contract(off)
   __shared__ double cs[64], sn[64];
-  const int e = a.pos[blockIdx.y];
+  const int e = a.index[blockIdx.y];
   const int tid = threadIdx.x;
-  const u32x4* src = reinterpret_cast<const u32x4*>(a.kv_layer_base + size_t(a.order[e]) * a.slot_stride);
-  u32x4* dst = reinterpret_cast<u32x4*>(a.view + size_t(e) * a.blk_stride);
+  const u32x4* src = reinterpret_cast<const u32x4*>(a.kv_layer_base + size_t(a.slot[blockIdx.y]) * a.slot_stride);
+  u32x4* dst = reinterpret_cast<u32x4*>(a.view + size_t(a.slot[blockIdx.y]) * a.blk_stride);
   const int64_t stride = int64_t(gridDim.x) * 256;
   if (tid < a.pairs) {
     const double w = pow(a.theta, -double(tid) / double(a.pairs));
@@ -698,7 +705,17 @@ __global__ __launch_bounds__(256) void rope_view_kernel(RopeViewArgs a) {
   __syncthreads();
   constexpr int kElts = BF16 ? 8 : 4;  // elements per 16-byte unit (whole pairs)
   const int units_per_head = a.head_dim / kElts;
-  for (int64_t u = int64_t(blockIdx.x) * 256 + tid; u < a.units; u += stride) {
+  const int t_units = (2 * a.pairs + kElts - 1) / kElts;  // units of a head holding temporal pairs
+  const bool full = a.full[blockIdx.y] != 0;
+  const int per_row = a.heads * (full ? units_per_head : t_units);
+  const int64_t count = a.rows * per_row;
+  for (int64_t i = int64_t(blockIdx.x) * 256 + tid; i < count; i += stride) {
+    int64_t u = i;
+    if (!full) {  // i-th temporal unit -> its unit in the block
+      const int64_t row = i / per_row;
+      const int r = int(i - row * per_row);
+      u = (row * a.heads + r / t_units) * units_per_head + r % t_units;
+    }
     u32x4 x = __builtin_nontemporal_load(src + u);
     const int d0 = int(u % units_per_head) * kElts;  // first element of the unit within its head
     if (d0 < 2 * a.pairs) {
@@ -822,6 +839,7 @@ void mirror_reset(fademem_cache* c) {
   const size_t views = c->cfg.rope_pairs > 0 ? size_t(c->cfg.layers) * size_t(c->lay.slots) : 0;
   c->view_first.assign(views, 0);
   c->view_span.assign(views, 0);
+  c->view_index.assign(views, -1);
 }
 
 // insert_kernel: the new entry goes to slot order[count].
@@ -1224,51 +1242,59 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
   return finish(c, stream);
 }
 
-// Rebuild the stale positions of layer `layer`'s re-indexed K view: the
-// first `held` positions are memory entries (rebuilt when the entry's
-// covered range changed since the last build), the `staged` after them are
-// staged frames (always rebuilt: their contents are the caller's).
+// Bring layer `layer`'s re-indexed K view up to date for the first `held`
+// entries (memory) and the `staged` after them (staged frames): a slot whose
+// entry changed is rewritten in full, a slot whose entry only moved to
+// another index has its temporal units rotated again; staged frames are
+// always rewritten in full (their contents are the caller's).
 int refresh_view(fademem_cache* c, int32_t layer, int held, int staged, void* stream) {
   const size_t base = size_t(layer) * size_t(c->lay.slots);
-  std::vector<int32_t> todo;
-  try {
-    todo.reserve(size_t(held + staged));
-  } catch (...) {
-    return FADEMEM_ENOMEM;
-  }
-  for (int i = 0; i < held; ++i) {
-    if (c->view_first[base + i] != c->mirror.first[size_t(i)] || c->view_span[base + i] != c->mirror.span[size_t(i)])
-      todo.push_back(i);
-  }
-  for (int i = held; i < held + staged; ++i) todo.push_back(i);
-  if (todo.empty()) return FADEMEM_OK;
   RopeViewArgs r;
   r.kv_layer_base = c->pool + kv_offset(c->lay, layer, 0, 0);
-  r.order = reinterpret_cast<const int32_t*>(c->pool + c->lay.off_order[c->cur]);
   r.view = c->pool + c->lay.off_view + base * c->lay.blk_stride;
   r.slot_stride = 2 * c->lay.blk_stride;
   r.blk_stride = c->lay.blk_stride;
-  r.units = int64_t(c->lay.blk_bytes / 16);
+  r.rows = c->cfg.tokens_per_block;
+  r.heads = c->cfg.heads;
   r.head_dim = c->cfg.head_dim;
   r.pairs = c->cfg.rope_pairs;
   r.theta = c->cfg.rope_theta;
+  r.n_pos = 0;
   auto vk = c->cfg.dtype == FADEMEM_BF16 ? rope_view_kernel<true> : rope_view_kernel<false>;
-  for (size_t p0 = 0; p0 < todo.size(); p0 += kMaxViewPos) {
-    const int np = int(todo.size() - p0 < size_t(kMaxViewPos) ? todo.size() - p0 : size_t(kMaxViewPos));
-    r.n_pos = np;
-    for (int i = 0; i < np; ++i) r.pos[i] = todo[p0 + i];
-    const dim3 grid(stream_blocks_per_plane(reinterpret_cast<const void*>(vk), unsigned(np), r.units, 4),
-                    unsigned(np));
+  const int64_t units = int64_t(c->lay.blk_bytes / 16);
+  auto flush = [&]() -> int {
+    if (r.n_pos == 0) return FADEMEM_OK;
+    const dim3 grid(stream_blocks_per_plane(reinterpret_cast<const void*>(vk), unsigned(r.n_pos), units, 4),
+                    unsigned(r.n_pos));
     hipLaunchKernelGGL(vk, grid, dim3(256), 0, as_stream(stream), r);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(c, e);
+    r.n_pos = 0;
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? FADEMEM_OK : hip_fail(c, e);
+  };
+  auto add = [&](int i, int32_t slot, bool full) -> int {
+    r.index[r.n_pos] = i;
+    r.slot[r.n_pos] = slot;
+    r.full[r.n_pos] = full ? 1 : 0;
+    return ++r.n_pos == kMaxViewPos ? flush() : FADEMEM_OK;
+  };
+  for (int i = 0; i < held + staged; ++i) {
+    const int32_t slot = c->mirror.order[size_t(i)];
+    const size_t v = base + size_t(slot);
+    int rc = FADEMEM_OK;
+    if (i >= held) {
+      rc = add(i, slot, true);
+      c->view_span[v] = 0;  // rebuilt on every use
+    } else if (c->view_first[v] != c->mirror.first[size_t(i)] || c->view_span[v] != c->mirror.span[size_t(i)]) {
+      rc = add(i, slot, true);
+      c->view_first[v] = c->mirror.first[size_t(i)];
+      c->view_span[v] = c->mirror.span[size_t(i)];
+    } else if (c->view_index[v] != i) {
+      rc = add(i, slot, false);
+    }
+    c->view_index[v] = i;
+    if (rc) return rc;
   }
-  for (int i = 0; i < held; ++i) {
-    c->view_first[base + i] = c->mirror.first[size_t(i)];
-    c->view_span[base + i] = c->mirror.span[size_t(i)];
-  }
-  for (int i = held; i < held + staged; ++i) c->view_span[base + i] = 0;  // rebuilt on every use
-  return FADEMEM_OK;
+  return flush();
 }
 
 // Attention over [memory || staged frames || current chunk] (the staged
@@ -1310,11 +1336,11 @@ int attend_impl(fademem_cache* c, int32_t layer, const void* q, int64_t q_tokens
   (void)hipGetLastError();
   if (c->cfg.rope_pairs > 0 && entries > 0) {
     // Expose the memory re-indexed: keys from the layer's rotated K view
-    // (entry e at view position e), values from the slots as stored.
+    // (one block per slot, read through the slot table), values from the
+    // slots as stored.
     const int rc = refresh_view(c, layer, int(c->count), int(staged), stream);
     if (rc) return rc;
     a.k_base = c->pool + c->lay.off_view + size_t(layer) * size_t(c->lay.slots) * c->lay.blk_stride;
-    a.k_order = nullptr;
     a.k_stride = c->lay.blk_stride;
   }
   hipError_t e = (c->cfg.dtype == FADEMEM_BF16) ? launch_attend_bf16(a, as_stream(stream))
