@@ -53,7 +53,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 # split tiles) at the wan1.3b-1layer workload, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE (see profiles/attend_bf16_wan1.3b_1layer.md), valid only for the
 # kernel source they were taken on (first 16 hex digits of its sha256).
-ATTN_TRAFFIC = {"source_sha256": "7286bd87b8468878", "workload": "wan1.3b-1layer", "bytes_per_call": 761847800}
+ATTN_TRAFFIC = {"source_sha256": "591558dd237ae592", "workload": "wan1.3b-1layer", "bytes_per_call": 758653440}
 
 
 # HBM bytes of one fused chunk update's data pass (update_data_kernel) in
@@ -106,6 +106,7 @@ def parse():
     p.add_argument("--denoise-steps", type=int, default=1,
                    help="attention calls per layer per chunk (the generator's sampler calls it once per denoising "
                         "step on the same memory; the update follows the last step)")
+    p.add_argument("--lse", action="store_true", help="have every attention call also return the log-sum-exp")
     p.add_argument("--rope-pairs", type=int, default=0,
                    help="temporal RoPE handling: pairs of each head carrying the temporal phase (Wan-class: 22 of "
                         "64); the memory is exposed re-indexed (0 = off)")
@@ -369,6 +370,7 @@ def main():
             per_layer.append((q.to(tdtype), k.to(tdtype).contiguous(), v.to(tdtype).contiguous()))
         inputs.append(per_layer)
     out = torch.empty((F * N, H, D), dtype=tdtype, device=dev)
+    lse = torch.empty((H, F * N), dtype=torch.float32, device=dev) if args.lse else None
     cache = Cache(budget=M, heads=H, head_dim=D, tokens_per_block=N, beta=args.beta, anchor=anchor,
                   dtype=tdtype, layers=L, device=dev, merge_op=args.merge_op, rope_pairs=args.rope_pairs)
     torch.cuda.synchronize()
@@ -388,7 +390,7 @@ def main():
                     ev["attn"].append(new_pair())
                     ev["attn"][-1][0].record(stream)
                     ev["keys"].append(cache.count() * N + F * N)  # host mirror of the count: no sync
-                cache.attend(q, k, v, layer=l, out=out)
+                cache.attend(q, k, v, layer=l, out=out, lse=lse)
                 if ev is not None:
                     ev["attn"][-1][1].record(stream)
         if ev is not None:
@@ -514,7 +516,7 @@ def main():
                    "frames_per_chunk": F, "query_tokens": F * N, "budget": M, "beta": args.beta,
                    "anchor": anchor, "merge_op": args.merge_op, "layers": L, "chunks": chunks,
                    "update": args.update, "denoise_steps": args.denoise_steps, "rope_pairs": args.rope_pairs,
-                   "keys_per_attend": lk},
+                   "lse": args.lse, "keys_per_attend": lk},
         "attention_tflops": round(attn_tflops, 2),
         "attention_ms_per_call": round(attn_avg_s * 1e3, 4),
         "update": args.update,

@@ -39,10 +39,11 @@
 //   last key again and score -inf.
 // * Online softmax in base 2 with the scale folded into one FMA; O is
 //   rescaled only when a row max grows by more than 2^8 (the stale max
-//   cancels in the final normalisation).  O's denominator sums the
-//   bf16-rounded weights that enter the P.V product; when the caller asks
-//   for the log-sum-exp, a second fp32 sum of the unrounded weights gives
-//   it (the kernel variant without LSE output skips that sum).
+//   cancels in the final normalisation).  The row sum adds the fp32
+//   weights before their bf16 rounding for the P.V product: it normalises O
+//   (within 2^-9 of the rounded weights' sum) and gives the log-sum-exp
+//   exact to fp32 rounding.  Two plain adds per pair of weights cost less
+//   beside the MFMAs than summing the rounded pair with a v_dot2.
 // * Workgroup index -> work is remapped so that one XCD runs a contiguous
 //   range of (head, query tile) and shares K/V in its L2.
 #include <mutex>
@@ -121,15 +122,11 @@ __device__ __forceinline__ int vswz(int n) {
   return 4 * ((n / Shape<D>::RPB) % (4 / Shape<D>::RPB));
 }
 
-// Round two weights to bf16 and add the ROUNDED values to an fp32 sum in one
-// v_dot2 against (1, 1): the denominator then sums exactly the weights the
-// P.V product uses, so O is a convex combination of V rows.
-__device__ __forceinline__ uint32_t round_and_sum(float p0, float p1, float& sum) {
+// Two weights rounded to bf16 and packed as one B-operand word of P.V.
+__device__ __forceinline__ uint32_t round_pair(float p0, float p1) {
   bf16x2 pk;
   pk[0] = (__bf16)p0;
   pk[1] = (__bf16)p1;
-  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  sum = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, sum, false);
   return __builtin_bit_cast(uint32_t, pk);
 }
 
@@ -163,7 +160,7 @@ __device__ __forceinline__ int xcd_group(int bid, int groups) {
 // LSE.
 template <int D>
 __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (&o)[Shape<D>::DB], float m_scaled,
-                                          float l_tot, float l_lse, int q_row, int h, int hh) {
+                                          float l_tot, int q_row, int h, int hh) {
   const int H = args.heads;
   const int Lq = int(args.q_tokens);
   if (q_row >= Lq) return;
@@ -179,17 +176,17 @@ __device__ __forceinline__ void store_out(const AttendArgs& args, const f32x16 (
       const int d = 32 * db + 8 * g4 + 4 * hh;
       *reinterpret_cast<bf16x4*>(obase + d * 2) = v;
     }
-  if (args.lse && hh == 0) args.lse[size_t(h) * Lq + q_row] = (m_scaled + __log2f(l_lse)) * kLn2;
+  if (args.lse && hh == 0) args.lse[size_t(h) * Lq + q_row] = (m_scaled + __log2f(l_tot)) * kLn2;
 }
 
 // Scratch slot layout of a partial result: O registers lane-major,
-// [wave][qb][db][r][lane], then m, l and the unrounded sum per (qb, thread).
+// [wave][qb][db][r][lane], then m and l per (qb, thread).
 template <int D>
 __device__ __forceinline__ size_t ws_o_index(int wave, int qb, int db, int r, int lane) {
   return ((size_t((wave * QB + qb) * Shape<D>::DB + db) * 16 + r) * 64 + lane);
 }
 
-template <int D, bool WIDE, bool LSE>
+template <int D, bool WIDE>
 __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const SkPlan& plan) {
   using S = Shape<D>;
   // Three-deep rings of K and V tile buffers, each a separate LDS object.
@@ -407,19 +404,17 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
       for (int db = 0; db < S::DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[qb][db][r] = 0.0f;
-    float m_run[QB], l_run[QB], lu_run[QB];
+    float m_run[QB], l_run[QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       m_run[qb] = -INFINITY;  // running (possibly stale) max of raw scores
-      l_run[qb] = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2), rounded to bf16
-      lu_run[qb] = 0.0f;      // the same sum of the unrounded weights (LSE only)
+      l_run[qb] = 0.0f;       // this lane's partial sum of 2^(s*c2 - m_run*c2)
     }
 
     const int partial_tile = (Lk % kBN) ? (Lk / kBN) : -1;  // the tile with keys >= Lk, if any
     f32x16 s_cur[2][QB];  // S^T of the current tile [nb][qb]
     u32x4 p_cur[4][QB];   // P of the current tile [ks][qb] (bf16 pairs)
-    float ps_cur[QB];     // this lane's sum of the current tile's P so far
-    float pu_cur[QB];     // the same of the unrounded weights (LSE only)
+    float ps_cur[QB];     // this lane's sum of the current tile's weights so far
 
     // Softmax without a per-tile row max: a tile's weights are taken against
     // the running max m_run as it stands.  If any weight of a row exceeds
@@ -433,13 +428,13 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     // in block B, the rest in the next block A.
     constexpr int kPairs = 16 * QB;
     constexpr int kPairsB = 8 * QB;
-    auto exp_pair = [&](const f32x16 (&s)[2][QB], u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB], int pi) {
+    auto exp_pair = [&](const f32x16 (&s)[2][QB], u32x4 (&p)[4][QB], float (&ps)[QB], int pi) {
       const int qb = pi / 16, rr = pi % 16, nb = rr / 8, r = 2 * (rr % 8);
       const float mc = m_run[qb] * c2;
       const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r], c2, -mc));
       const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[nb][qb][r + 1], c2, -mc));
-      if constexpr (LSE) pu[qb] = (pu[qb] + p0) + p1;
-      const uint32_t w = round_and_sum(p0, p1, ps[qb]);
+      ps[qb] = ps[qb] + (p0 + p1);
+      const uint32_t w = round_pair(p0, p1);
       asm volatile("" ::"v"(w));  // keep the weight in its pipeline step
       p[2 * nb + (r >> 3)][qb][(r & 7) >> 1] = w;
     };
@@ -494,7 +489,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     // Redo a tile against the exact running max: its scores again from its K
     // buffer, new m_run, rescale O and l, recompute all its weights and the
     // tile sum.
-    auto redo_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB]) {
+    auto redo_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
       f32x16 s[2][QB];
       qk_tile(tile, kb_lds, s);
       float mx[QB];
@@ -505,28 +500,25 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         const float alpha = __builtin_amdgcn_exp2f((m_run[qb] - m_new) * c2);
         m_run[qb] = m_new;
         l_run[qb] *= alpha;
-        if constexpr (LSE) lu_run[qb] *= alpha;
 #pragma unroll
         for (int db = 0; db < S::DB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[qb][db][r] *= alpha;
         ps[qb] = 0.0f;
-        pu[qb] = 0.0f;
       }
 #pragma unroll
-      for (int pi = 0; pi < kPairs; ++pi) exp_pair(s, p, ps, pu, pi);
+      for (int pi = 0; pi < kPairs; ++pi) exp_pair(s, p, ps, pi);
     };
     // End of a tile's weights: redo it if a weight grew past 2^8, then add
     // its sum to l.
-    auto close_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB], float (&pu)[QB]) {
+    auto close_tile = [&](int tile, const char* kb_lds, u32x4 (&p)[4][QB], float (&ps)[QB]) {
       bool grow = false;
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) grow = grow || !(ps[qb] <= kRescaleBound);
-      if (__any(grow)) redo_tile(tile, kb_lds, p, ps, pu);
+      if (__any(grow)) redo_tile(tile, kb_lds, p, ps);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         l_run[qb] += ps[qb];
-        if constexpr (LSE) lu_run[qb] += pu[qb];
       }
     };
     auto read_k = [&](const char* kb_lds, int kb, bf16x8 (&kf)[2]) {
@@ -608,10 +600,10 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         }
 #pragma unroll
         for (int pi = kPairsB; pi < kPairs; ++pi)
-          if (st == (pi - kPairsB) * S::KB / (kPairs - kPairsB)) exp_pair(s_cur, p_cur, ps_cur, pu_cur, pi);
+          if (st == (pi - kPairsB) * S::KB / (kPairs - kPairsB)) exp_pair(s_cur, p_cur, ps_cur, pi);
         __builtin_amdgcn_sched_barrier(0);
       }
-      close_tile(t, kbuf[b], p_cur, ps_cur, pu_cur);  // tile t's K buffer is refilled only in the next block A
+      close_tile(t, kbuf[b], p_cur, ps_cur);  // tile t's K buffer is refilled only in the next block A
       __builtin_amdgcn_sched_barrier(0);
 
       // Block B: O += V(t) P(t), two 32-row blocks of one k-step per step,
@@ -620,12 +612,9 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         if (maskn) mask(t + 1, s_next);
       }
       u32x4 p_next[4][QB];
-      float ps_next[QB], pu_next[QB];
+      float ps_next[QB];
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        ps_next[qb] = 0.0f;
-        pu_next[qb] = 0.0f;
-      }
+      for (int qb = 0; qb < QB; ++qb) ps_next[qb] = 0.0f;
 #pragma unroll
       for (int st = 0; st < kStepsB; ++st) {
         const int ks = st / (S::DB / kDbPerStep), db0 = (st % (S::DB / kDbPerStep)) * kDbPerStep;
@@ -645,7 +634,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
         if constexpr (NEXT) {
 #pragma unroll
           for (int pi = 0; pi < kPairsB; ++pi)
-            if (st == pi * kStepsB / kPairsB) exp_pair(s_next, p_next, ps_next, pu_next, pi);
+            if (st == pi * kStepsB / kPairsB) exp_pair(s_next, p_next, ps_next, pi);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -659,7 +648,6 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
 #pragma unroll
           for (int ks = 0; ks < 4; ++ks) p_cur[ks][qb] = p_next[ks][qb];
           ps_cur[qb] = ps_next[qb];
-          pu_cur[qb] = pu_next[qb];
         }
       }
     };
@@ -675,12 +663,9 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
       qk_tile(kt0, kbuf[0], s_cur);
       row_max(s_cur, m_run);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        ps_cur[qb] = 0.0f;
-        pu_cur[qb] = 0.0f;
-      }
+      for (int qb = 0; qb < QB; ++qb) ps_cur[qb] = 0.0f;
 #pragma unroll
-      for (int pi = 0; pi < kPairsB; ++pi) exp_pair(s_cur, p_cur, ps_cur, pu_cur, pi);
+      for (int pi = 0; pi < kPairsB; ++pi) exp_pair(s_cur, p_cur, ps_cur, pi);
     }
 
     using I0 = std::integral_constant<int, 0>;
@@ -719,8 +704,7 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     if (slot < 0) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
-        store_out<D>(args, o[qb], m_run[qb] * c2, pair_sum(l_run[qb]), LSE ? pair_sum(lu_run[qb]) : 1.0f,
-                     qt * kBM + wave * kQW + 32 * qb + l32, h, hh);
+        store_out<D>(args, o[qb], m_run[qb] * c2, pair_sum(l_run[qb]), qt * kBM + wave * kQW + 32 * qb + l32, h, hh);
     } else {
       float* ws = args.ws + size_t(slot) * attend_slot_floats(D);
 #pragma unroll
@@ -731,7 +715,6 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
           for (int r = 0; r < 16; ++r) ws[ws_o_index<D>(wave, qb, db, r, lane)] = o[qb][db][r];
         ws[kBM * D + qb * kThreads + tid] = m_run[qb];
         ws[kBM * D + (QB + qb) * kThreads + tid] = l_run[qb];
-        if constexpr (LSE) ws[kBM * D + (2 * QB + qb) * kThreads + tid] = lu_run[qb];
       }
     }
   };
@@ -781,57 +764,42 @@ __device__ __forceinline__ void attend_bf16_merge_body(const AttendArgs& args, c
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int mi = kBM * D + qb * kThreads + tid, li = kBM * D + (QB + qb) * kThreads + tid;
-    const int ui = kBM * D + (2 * QB + qb) * kThreads + tid;
     const float m_max = fmaxf(part[0][mi], part[1][mi]);
     f32x16 o[S::DB];
 #pragma unroll
     for (int db = 0; db < S::DB; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
-    float l_tot = 0.0f, l_lse = 0.0f;
+    float l_tot = 0.0f;
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
       const float* ws = part[p];
       const float f = __builtin_amdgcn_exp2f((ws[mi] - m_max) * c2);
       l_tot += f * pair_sum(ws[li]);
-      if (args.lse) l_lse += f * pair_sum(ws[ui]);
 #pragma unroll
       for (int db = 0; db < S::DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] += f * ws[ws_o_index<D>(wave, qb, db, r, lane)];
     }
-    store_out<D>(args, o, m_max * c2, l_tot, l_lse, (qg % plan.q_tiles) * kBM + wave * kQW + 32 * qb + l32,
+    store_out<D>(args, o, m_max * c2, l_tot, (qg % plan.q_tiles) * kBM + wave * kQW + 32 * qb + l32,
                  qg / plan.q_tiles, hh);
   }
 }
 
 }  // namespace
 
-// Kernels: head dimension, entries of at least one key tile (or shorter),
-// with or without the log-sum-exp output.
+// Kernels: head dimension, entries of at least one key tile (or shorter).
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, true, false>(args, plan);
+  attend_bf16_body<128, true>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, true, false>(args, plan);
+  attend_bf16_body<64, true>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_short(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, false, false>(args, plan);
+  attend_bf16_body<128, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_short(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, false, false>(args, plan);
-}
-__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_lse(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, true, true>(args, plan);
-}
-__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_lse(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, true, true>(args, plan);
-}
-__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d128_short_lse(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<128, false, true>(args, plan);
-}
-__global__ __launch_bounds__(kThreads, 1) void attend_bf16_d64_short_lse(AttendArgs args, SkPlan plan) {
-  attend_bf16_body<64, false, true>(args, plan);
+  attend_bf16_body<64, false>(args, plan);
 }
 __global__ __launch_bounds__(kThreads) void attend_bf16_merge_d128(AttendArgs args, SkPlan plan) {
   attend_bf16_merge_body<128>(args, plan);
@@ -893,20 +861,16 @@ hipError_t launch_d(AttnKernel kernel, AttnKernel merge, std::once_flag& attr_on
   return e;
 }
 
-std::once_flag attr_once[8];
+std::once_flag attr_once[4];
 
 }  // namespace
 
 hipError_t launch_attend_bf16(const AttendArgs& a, hipStream_t stream) {
-  const bool wide = a.tokens_per_block >= kBN;
-  const bool lse = a.lse != nullptr;
-  static const AttnKernel k128[2][2] = {{attend_bf16_d128_short, attend_bf16_d128_short_lse},
-                                        {attend_bf16_d128, attend_bf16_d128_lse}};
-  static const AttnKernel k64[2][2] = {{attend_bf16_d64_short, attend_bf16_d64_short_lse},
-                                       {attend_bf16_d64, attend_bf16_d64_lse}};
-  const int w = wide ? 1 : 0, l = lse ? 1 : 0;
-  if (a.head_dim == 128) return launch_d(k128[w][l], attend_bf16_merge_d128, attr_once[w * 2 + l], a, stream);
-  if (a.head_dim == 64) return launch_d(k64[w][l], attend_bf16_merge_d64, attr_once[4 + w * 2 + l], a, stream);
+  const int w = a.tokens_per_block >= kBN ? 1 : 0;
+  static const AttnKernel k128[2] = {attend_bf16_d128_short, attend_bf16_d128};
+  static const AttnKernel k64[2] = {attend_bf16_d64_short, attend_bf16_d64};
+  if (a.head_dim == 128) return launch_d(k128[w], attend_bf16_merge_d128, attr_once[w], a, stream);
+  if (a.head_dim == 64) return launch_d(k64[w], attend_bf16_merge_d64, attr_once[2 + w], a, stream);
   return hipErrorInvalidValue;
 }
 

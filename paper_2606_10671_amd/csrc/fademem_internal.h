@@ -28,10 +28,9 @@ constexpr int kAttnThreads = 512;        // threads per workgroup (8 waves)
 constexpr int kAttnQueries = 256;        // queries per workgroup (32 per wave)
 constexpr int kSkMaxGroups = 256;        // workgroups of one launch at most (one per CU)
 __host__ __device__ constexpr size_t attend_slot_floats(int head_dim) {
-  // O of every query, then the row max, the partial row sum of the rounded
-  // weights and that of the unrounded weights (kept for the LSE) of every
+  // O of every query, then the row max and the partial row sum of every
   // (thread, 32-query block).
-  return size_t(kAttnQueries) * size_t(head_dim) + 6 * size_t(kAttnQueries);
+  return size_t(kAttnQueries) * size_t(head_dim) + 4 * size_t(kAttnQueries);
 }
 __host__ __device__ constexpr size_t attend_ws_bytes(int head_dim) {
   return 2 * size_t(kSkMaxGroups) * attend_slot_floats(head_dim) * sizeof(float);

@@ -49,19 +49,19 @@ GOOD = dict(budget=21, heads=12, head_dim=128, tokens_per_block=1560, beta=0.3, 
 def test_pool_bytes_layout():
     """Metadata (< 64 KiB) + (M+1) K and V slots per layer; bf16 caches add
     the attention's split-work scratch: two slots per workgroup (at most
-    256) of 256 queries x D fp32 partial O plus 1536 fp32 maxima and sums
-    (the same bytes as 512 slots of 128 queries x D plus 768 floats); fp32
+    256) of 256 queries x D fp32 partial O plus 1024 fp32 maxima and sums
+    (the same bytes as 512 slots of 128 queries x D plus 512 floats); fp32
     caches add 512 slots of 64 queries x (D + 2) floats for key ranges."""
     n = fm.fademem_pool_bytes(fm.make_config(**GOOD))
     blk = 1560 * 12 * 128 * 2
-    ws = 2 * 512 * (128 * 128 + 3 * 256) * 4
+    ws = 2 * 512 * (128 * 128 + 2 * 256) * 4
     assert n >= 22 * 2 * blk + ws and n < 22 * 2 * blk + ws + 64 * 1024
     n30 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "layers": 30}))
     assert n30 - n == 29 * 22 * 2 * blk
     nf = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "dtype": fm.FADEMEM_F32}))
     assert nf - n == 22 * 2 * blk - ws + 512 * 64 * (128 + 2) * 4
     n64 = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "head_dim": 64}))
-    assert n - n64 == 22 * blk + ws - 2 * 512 * (128 * 64 + 3 * 256) * 4
+    assert n - n64 == 22 * blk + ws - 2 * 512 * (128 * 64 + 2 * 256) * 4
     # staging three frames: M + 3 slots per layer instead of M + 1
     ns = fm.fademem_pool_bytes(fm.make_config(**{**GOOD, "stage_frames": 3}))
     assert ns - n == 2 * 2 * blk

@@ -82,8 +82,8 @@ def test_bf16_wan_heads_small_tokens():
 
 @pytest.mark.parametrize("N", [200, 40])
 def test_lse_request_leaves_the_output_unchanged(N):
-    """The kernel variant that also returns the log-sum-exp keeps a second
-    sum of the unrounded weights; O must be the same bits either way."""
+    """Asking for the log-sum-exp adds only its store: O must be the same
+    bits either way."""
     import torch
     from paper_2606_10671_amd.fademem import Cache
     H, D, F, M = 2, 128, 3, 5
