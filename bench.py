@@ -60,7 +60,7 @@ ATTN_TRAFFIC = {"source_sha256": "591558dd237ae592", "workload": "wan1.3b-1layer
 # the 30-layer update leg, from rocprofv3 FETCH_SIZE and WRITE_SIZE scaled
 # by the insert copy (see profiles/update_data_wan1.3b_30layer.md); valid
 # only for the cache.hip source they were taken on.
-UPD_TRAFFIC = {"source_sha256": "9f62f9b86a4cf442", "workload": "wan1.3b-30layer-update", "bytes_per_call": 4259776784}
+UPD_TRAFFIC = {"source_sha256": "7e01d55b59f6f192", "workload": "wan1.3b-30layer-update", "bytes_per_call": 4259803392}
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.

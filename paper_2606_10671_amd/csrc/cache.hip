@@ -582,8 +582,9 @@ struct UpdateDataArgs {
   int64_t units;   // 16-byte units per K (or V) block
 };
 
-// grid.y = layer * 2 + kv: the blocks of a (layer, K|V) plane stride over
-// it, every plane of the launch streamed at once.
+// grid.y = layer * 2 + kv: the blocks of a (layer, K|V) plane cover it,
+// one 16-byte unit per thread (striding on if the plane needs more blocks
+// than a grid row holds).
 template <bool BF16, bool MAXOP>
 __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
   constexpr int kM = kMaxPlanFrames, kO = 2 * kMaxPlanFrames;
