@@ -64,7 +64,7 @@ UPD_TRAFFIC = {"source_sha256": "7e01d55b59f6f192", "workload": "wan1.3b-30layer
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.
-SPEC_TRAFFIC = {"source_sha256": "9ead68d6867c130d", "workload": "spectral-374clips", "bytes_per_call": 1740288092}
+SPEC_TRAFFIC = {"source_sha256": "cdbe5ca3b4bd15d7", "workload": "spectral-374clips", "bytes_per_call": 1740286899}
 
 
 def measured_traffic(table, source, workload):
