@@ -393,13 +393,8 @@ def main():
                 cache.attend(q, k, v, layer=l, out=out, lse=lse)
                 if ev is not None:
                     ev["attn"][-1][1].record(stream)
-        if ev is not None:
-            ev["upd"].append(new_pair())
-            ev["upd"][-1][0].record(stream)
         if args.update == "fused":
             cache.update([per_layer[l][1] for l in range(L)], [per_layer[l][2] for l in range(L)], c * F)
-            if ev is not None:
-                ev["upd"][-1][1].record(stream)
             return
         for f in range(F):
             ks = [per_layer[l][1][f * N:(f + 1) * N] for l in range(L)]
@@ -415,25 +410,26 @@ def main():
             cache.consolidate()
             if ev is not None:
                 ev["cons"][-1][1].record(stream)
-        if ev is not None:
-            ev["upd"][-1][1].record(stream)
 
     for c in range(first_timed):
         chunk_step(c)
     torch.cuda.synchronize()
     merges_before, anchor_before = cache.merge_counts()
 
-    # ---- timed region: whole chunk steps, with events around every call on
-    # the stream the kernels run on (per-kernel averages come from these) -----
+    # ---- timed region: whole chunk steps, with events around every attention
+    # call on the stream the kernels run on (per-kernel averages come from
+    # these).  Each recorded event leaves the GPU idle for a few microseconds,
+    # so chunk and update times are read off the attention events instead of
+    # events of their own: a chunk starts at its first attention call's start
+    # event, and its update runs from its last attention call's end event to
+    # the next chunk's start (so the update time includes the gaps of those
+    # two events) ----------------------------------------------------------
     t_start, t_end = new_pair()
-    ev = {"attn": [], "keys": [], "ins": [], "cons": [], "upd": []}
-    marks = []
+    ev = {"attn": [], "keys": [], "ins": [], "cons": []}
     torch.cuda.synchronize()
     t_start.record(stream)
     t_prog = time.time()
     for c in range(first_timed, chunks):
-        marks.append(torch.cuda.Event(enable_timing=True))
-        marks[-1].record(stream)
         chunk_step(c, ev)
         if time.time() - t_prog > 30:
             print(f"bench: chunk {c + 1}/{chunks} enqueued", file=sys.stderr, flush=True)
@@ -442,13 +438,15 @@ def main():
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_chunk = ms_total / args.steps
-    marks.append(t_end)
-    per_chunk = sorted(a.elapsed_time(b) for a, b in zip(marks[:-1], marks[1:]))
+    calls = args.denoise_steps * L  # attention calls per chunk
+    starts = [ev["attn"][i][0] for i in range(0, len(ev["attn"]), calls)] + [t_end]
+    ends = [ev["attn"][i + calls - 1][1] for i in range(0, len(ev["attn"]), calls)]
+    per_chunk = sorted(a.elapsed_time(b) for a, b in zip(starts[:-1], starts[1:]))
     ms_median = per_chunk[len(per_chunk) // 2]
     attn_ms = [a.elapsed_time(b) for a, b in ev["attn"]]
     ins_ms = [a.elapsed_time(b) for a, b in ev["ins"]]
     cons_ms = [a.elapsed_time(b) for a, b in ev["cons"]]
-    upd_ms = [a.elapsed_time(b) for a, b in ev["upd"]]
+    upd_ms = [a.elapsed_time(b) for a, b in zip(ends, starts[1:])]
     cache_timed = cache
 
     total_merges, anchor_total = cache_timed.merge_counts()
@@ -524,7 +522,8 @@ def main():
         "update_ms_per_chunk": round(sum(upd_ms) / len(upd_ms), 4),
         "update_gbps": round(update_gbps, 1) if update_gbps else None,
         "update_note": ("fused: algorithmic bytes of one pass (each operand block loaded once, each changed "
-                        "entry stored once) / time of the update call (plan + data kernels)"
+                        "entry stored once) / time from the chunk's last attention event to the next chunk's "
+                        "first (plan + data kernels and the idle gaps of those two timing events)"
                         if args.update == "fused" else "single: F x (insert + consolidate) per chunk"),
         "merge_gbps": round(merge_gbps, 1) if merge_gbps else None,
         "merge_note": "single-frame path only: algorithmic bytes of weighted merges / time of consolidate calls",
