@@ -53,7 +53,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # dense fp32 matrix-core peak (same figure as the
 # split tiles) at the wan1.3b-1layer workload, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE (see profiles/attend_bf16_wan1.3b_1layer.md), valid only for the
 # kernel source they were taken on (first 16 hex digits of its sha256).
-ATTN_TRAFFIC = {"source_sha256": "591558dd237ae592", "workload": "wan1.3b-1layer", "bytes_per_call": 758653440}
+ATTN_TRAFFIC = {"source_sha256": "a3f76e85dfec4181", "workload": "wan1.3b-1layer", "bytes_per_call": 1034552248}
 
 
 # HBM bytes of one fused chunk update's data pass (update_data_kernel) in

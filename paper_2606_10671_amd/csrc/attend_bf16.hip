@@ -46,6 +46,9 @@
 //   beside the MFMAs than summing the rounded pair with a v_dot2.
 // * Workgroup index -> work is remapped so that one XCD runs a contiguous
 //   range of (head, query tile) and shares K/V in its L2.
+// * In a head's last query tile, usually partial, the waves whose 32
+//   queries all lie past the last one only issue their share of the tile
+//   loads and meet the barriers: no MFMAs, no softmax, no result.
 #include <mutex>
 #include <type_traits>
 
@@ -397,6 +400,27 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
     };
     auto issue_tile = [&](int tile, char* kb_lds, char* vb_lds) { load_tile(tile_rows(tile), kb_lds, vb_lds); };
 
+    // A wave whose queries all lie past the last one (the last query tile
+    // of a head is usually partial) does no arithmetic: it issues its share
+    // of every tile's loads and meets the same barriers as the other waves
+    // (two in the prologue, one per key tile), and leaves no result.
+    if (qt * kBM + wave * kQW >= Lq) {
+      __syncthreads();
+      issue_tile(kt0, kbuf[0], vbuf[0]);
+      if (kt0 + 1 < kt1) issue_tile(kt0 + 1, kbuf[1], vbuf[1]);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      int b = 2;
+      for (int t = kt0; t < kt1; ++t) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (t + 2 < kt1)
+          issue_tile(t + 2, b == 0 ? kbuf[0] : b == 1 ? kbuf[1] : kbuf[2], b == 0 ? vbuf[0] : b == 1 ? vbuf[1] : vbuf[2]);
+        b = b == 2 ? 0 : b + 1;
+      }
+      return;
+    }
+
     f32x16 o[QB][S::DB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
@@ -747,7 +771,9 @@ __device__ __forceinline__ void attend_bf16_body(const AttendArgs& args, const S
 }
 
 // Merge of split query tiles: block i combines remaining tile i's head part
-// (slot i) and tail part (slot rem + i) and writes the output.
+// (slot i) and tail part (slot rem + i) and writes the output.  The slot
+// rows of waves past the last query hold no result; they are read but
+// never stored.
 template <int D>
 __device__ __forceinline__ void attend_bf16_merge_body(const AttendArgs& args, const SkPlan& plan) {
   using S = Shape<D>;
