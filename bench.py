@@ -12,14 +12,18 @@ single-layer workload (12 heads x 128, 1560 tokens per latent frame,
 3-frame chunks, budget 21, beta 0.3, anchor on, bf16).  Before the warm-up,
 ceil(M/F) + 1 fill chunks bring the memory to its steady state (full, with
 merges every frame), so every timed chunk attends over M*N + F*N keys and
-runs F merges whatever --warmup says; then the warm-up chunks and the timed
-chunks (8 + 112 by default).  After the headline chunks, a 30-layer leg
+runs F merges whatever --warmup says; then the warm-up chunks, untimed
+settle chunks until the warm-up and settle chunks have lasted --settle
+seconds (the chip's clock takes some tens of milliseconds of full load to
+settle), and the timed chunks (8 warm-up and 104 timed by default, about 300
+settle chunks at the default workload).  After the headline chunks, a 30-layer leg
 times the chunk update alone (fused, then zero-copy staged), whose working
 set is far above the 256 MB Infinity Cache: that is the merge's HBM
 roofline figure.
 """
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -93,6 +97,8 @@ def parse():
     p.add_argument("--steps", type=int, default=None,
                    help="timed chunks (default: the workload's chunk count minus the warm-up)")
     p.add_argument("--warmup", type=int, default=8)
+    p.add_argument("--settle", type=float, default=0.3,
+                   help="after the warm-up chunks, untimed chunks run until the load has lasted this many seconds")
     p.add_argument("--workload", default="wan1.3b-1layer", choices=sorted(WORKLOADS) + sorted(SPECTRAL))
     p.add_argument("--budget", type=int, default=None,
                    help="memory budget M in entries (default: the workload's; 12 is the paper's default, 15 slots with the current chunk)")
@@ -352,8 +358,7 @@ def main():
     fill = -(-M // F) + 1
     if args.steps is None:
         args.steps = max(1, wl["chunks"] - args.warmup - fill)
-    chunks = fill + args.warmup + args.steps
-    first_timed = fill + args.warmup
+    chunks = fill + args.warmup + args.steps  # settle chunks are added below
 
     # ---- inputs, resident in HBM before timing -------------------------------
     # Distinct chunks are generated up to ~16 GB and then reused cyclically
@@ -411,9 +416,29 @@ def main():
             if ev is not None:
                 ev["cons"][-1][1].record(stream)
 
-    for c in range(first_timed):
+    # Fill, warm-up, then settle chunks: the chip's clock takes some tens of
+    # milliseconds of full load to settle (a kernel trace shows the first
+    # attention calls over a full memory taking 1.17 ms, falling to 1.00 ms
+    # over about 20 calls), so untimed chunks run until the warm-up and
+    # settle chunks together have lasted --settle seconds, enqueued without
+    # gaps (their count comes from the warm-up chunks' pace).
+    for c in range(fill):
         chunk_step(c)
     torch.cuda.synchronize()
+    t_w = time.time()
+    warm = max(1, args.warmup)
+    for c in range(fill, fill + warm):
+        chunk_step(c)
+    torch.cuda.synchronize()
+    per_chunk_s = (time.time() - t_w) / warm
+    settle = 0
+    if per_chunk_s > 0 and args.settle > warm * per_chunk_s:
+        settle = min(4096, int(math.ceil((args.settle - warm * per_chunk_s) / per_chunk_s)))
+    for c in range(fill + warm, fill + warm + settle):
+        chunk_step(c)
+    torch.cuda.synchronize()
+    first_timed = fill + warm + settle
+    chunks = first_timed + args.steps
     merges_before, anchor_before = cache.merge_counts()
 
     # ---- timed region: whole chunk steps, with events around every attention
@@ -502,6 +527,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_chunks": settle,
         "fill_chunks": fill,
         "ms_per_step": round(ms_chunk, 4),
         "ms_per_chunk_median": round(ms_median, 4),
