@@ -57,7 +57,8 @@ def run_chunks(H, D, N, F, M, chunks, beta=0.3, anchor=True, layers=1, q_scale=1
 
 
 def test_bf16_d128_ragged():
-    # N = 200 rows per entry: tiles straddle entries; F*N = 600 queries = 4 tiles + 88 rows.
+    # N = 200 rows per entry: tiles straddle entries; F*N = 600 queries = 2 tiles of 256 + 88 rows, so in
+    # the last query tile waves 3-7 hold no query (they only load and meet the barriers).
     run_chunks(H=2, D=128, N=200, F=3, M=6, chunks=8)
 
 
