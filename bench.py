@@ -252,9 +252,10 @@ def update_leg(args, M, anchor, L=30, H=12, D=128, N=1560, F=3):
     (fademem_update: the caller's chunk is read, kept frames are copied into
     the pool) and as many zero-copy staged updates (fademem_update_staged:
     the chunk's frames are first written into the staging slots, as the
-    model's K/V projection would, outside the timed calls).  Events bracket
-    each update call on its stream; bytes are the algorithmic bytes replayed
-    from the logged merge decisions."""
+    model's K/V projection would, outside the timed calls).  One pair of
+    events brackets the back-to-back fused updates, a pair each staged update
+    call (the staging copies run between them); bytes are the algorithmic
+    bytes replayed from the logged merge decisions."""
     import torch
     from paper_2606_10671_amd.fademem import Cache
     from paper_2606_10671_amd.synth import TorchWanStream
@@ -284,25 +285,36 @@ def update_leg(args, M, anchor, L=30, H=12, D=128, N=1560, F=3):
     for mode in ("fused", "staged"):
         evs = []
         c0 = c
-        for _ in range(T):
-            d = data[c % distinct]
-            if mode == "staged":
+        if mode == "fused":
+            # Back-to-back updates between one pair of events (each recorded
+            # event leaves the GPU idle for a few microseconds).
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(T):
+                d = data[c % distinct]
+                cache.update([x[0] for x in d], [x[1] for x in d], c * F)
+                c += 1
+            e1.record(stream)
+            evs.append((e0, e1))
+        else:
+            # The staging copies (the model's projection writing the frames)
+            # run between the timed calls: a pair of events around each.
+            for _ in range(T):
+                d = data[c % distinct]
                 slots = cache.stage(F)
                 for l in range(L):
                     for f in range(F):
                         slots[l][f][0].copy_(d[l][0][f * N:(f + 1) * N])
                         slots[l][f][1].copy_(d[l][1][f * N:(f + 1) * N])
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            if mode == "fused":
-                cache.update([x[0] for x in d], [x[1] for x in d], c * F)
-            else:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
                 cache.update_staged(F, c * F)
-            e1.record(stream)
-            evs.append((e0, e1))
-            c += 1
+                e1.record(stream)
+                evs.append((e0, e1))
+                c += 1
         torch.cuda.synchronize()
-        ms = [a.elapsed_time(b) for a, b in evs]
+        ms_total = sum(a.elapsed_time(b) for a, b in evs)
+        ms = [ms_total / T] * T
         _, log = cache.merge_log(cap=4096)
         js = log[len(log) - T * F:]
         bytes_ = 0
