@@ -585,9 +585,11 @@ struct UpdateDataArgs {
 // grid.y = layer * 2 + kv: the blocks of a (layer, K|V) plane cover it,
 // one 16-byte unit per thread (striding on if the plane needs more blocks
 // than a grid row holds).
-template <bool BF16, bool MAXOP>
+template <bool BF16, bool MAXOP, int MF>
 __global__ __launch_bounds__(256) void update_data_kernel(UpdateDataArgs a) {
-  constexpr int kM = kMaxPlanFrames, kO = 2 * kMaxPlanFrames;
+  // Operand arrays for plans of up to MF frames: at most MF merges and 2 * MF
+  // entries written.
+  constexpr int kM = MF, kO = 2 * MF;
   const UpdatePlan* P = reinterpret_cast<const UpdatePlan*>(a.pool + a.lay.off_prog);
   const int n_ar = P->n_ar, n_out = P->n_out;
   // Result r of the merges computed so far (r is wave-uniform).
@@ -1197,8 +1199,20 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
   (void)hipGetLastError();
   const int64_t units = int64_t(c->lay.blk_bytes / 16);
   const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
-  auto data_kernel = bf16 ? (maxop ? update_data_kernel<true, true> : update_data_kernel<true, false>)
-                          : (maxop ? update_data_kernel<false, true> : update_data_kernel<false, false>);
+  // Fused updates launch the data kernel sized for kMaxPlanFrames frames;
+  // staged ones the instance sized for the plan's frames (fewer registers,
+  // more resident waves: 4% faster staged, 2% slower fused at 30 layers).
+  typedef void (*DataKernel)(UpdateDataArgs);
+  static_assert(kMaxPlanFrames == 4, "one data kernel per plan size");
+  static const DataKernel data_kernels[2][2][kMaxPlanFrames] = {
+      {{update_data_kernel<false, false, 1>, update_data_kernel<false, false, 2>, update_data_kernel<false, false, 3>,
+        update_data_kernel<false, false, 4>},
+       {update_data_kernel<false, true, 1>, update_data_kernel<false, true, 2>, update_data_kernel<false, true, 3>,
+        update_data_kernel<false, true, 4>}},
+      {{update_data_kernel<true, false, 1>, update_data_kernel<true, false, 2>, update_data_kernel<true, false, 3>,
+        update_data_kernel<true, false, 4>},
+       {update_data_kernel<true, true, 1>, update_data_kernel<true, true, 2>, update_data_kernel<true, true, 3>,
+        update_data_kernel<true, true, 4>}}};
   const unsigned per_plane = plane_blocks(units, 1);
   for (int64_t f0 = 0; f0 < frames; f0 += kMaxPlanFrames) {
     const int nf = int((frames - f0) < kMaxPlanFrames ? (frames - f0) : kMaxPlanFrames);
@@ -1231,6 +1245,7 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
       da.lay = c->lay;
       da.layer0 = l0;
       da.units = units;
+      const DataKernel data_kernel = data_kernels[bf16][maxop][staged ? nf - 1 : kMaxPlanFrames - 1];
       hipLaunchKernelGGL(data_kernel, dim3(per_plane, unsigned(2 * nl)), dim3(256), 0, as_stream(stream), da);
       e = hipGetLastError();
       if (e != hipSuccess) return hip_fail(c, e);
