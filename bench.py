@@ -154,15 +154,17 @@ def fused_block_ios(js, count0, F, M, anchor, merge_op, staged=False):
 
 def cpu_baseline(wl, head_inputs, beta, anchor, budget_s, merge_op="sqrt_span"):
     """The oracle, as it stands, on the host cores: one steady-state chunk
-    step (memory full, F merges), restricted to whole heads, as many heads
-    as fit the time budget, scaled to all heads and layers (the step is
-    independent per head and per layer)."""
+    step (memory full, F merges) per head, heads taken in turn (and again,
+    from a freshly filled memory, once all have run) until the time budget
+    is spent, scaled to all heads and layers (the step is independent per
+    head and per layer)."""
     from threadpoolctl import threadpool_info
     from oracle import OracleCache, chunk_step
 
     H, F = wl["heads"], wl["frames"]
     heads_done, t_total = 0, 0.0
-    for h in range(H):
+    while t_total < budget_s:
+        h = heads_done % H
         q, k, v, fill_k, fill_v = head_inputs(h)
         oc = OracleCache(budget=wl["budget"], beta=beta, anchor=anchor, storage=wl["dtype"], operator=merge_op)
         for t in range(len(fill_k)):          # fill the memory (untimed)
@@ -171,16 +173,14 @@ def cpu_baseline(wl, head_inputs, beta, anchor, budget_s, merge_op="sqrt_span"):
         chunk_step(oc, q, k, v, F, len(fill_k))
         t_total += time.perf_counter() - t0
         heads_done += 1
-        if t_total >= budget_s:
-            break
     ms_chunk = t_total / heads_done * H * 1e3 * wl["layers"]
     blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     return {
         "value": round(ms_chunk, 2), "unit": "ms/chunk", "cores": int(blas_threads), "kind": "oracle",
         "host_cpus": len(os.sched_getaffinity(0)),
         "sample": (f"one steady-state chunk step (fp64 attention over the full memory + {F} updates with "
-                   f"merges), {heads_done} of {H} heads of one layer, {t_total:.1f} s, scaled to {H} heads"
-                   + (f" x {wl['layers']} layers" if wl["layers"] > 1 else "")),
+                   f"merges) per head, {heads_done} head-steps of {H} heads of one layer, {t_total:.1f} s, "
+                   f"scaled to {H} heads" + (f" x {wl['layers']} layers" if wl["layers"] > 1 else "")),
     }
 
 
