@@ -64,7 +64,7 @@ ATTN_TRAFFIC = {"source_sha256": "a3f76e85dfec4181", "workload": "wan1.3b-1layer
 # the 30-layer update leg, from rocprofv3 FETCH_SIZE and WRITE_SIZE scaled
 # by the insert copy (see profiles/update_data_wan1.3b_30layer.md); valid
 # only for the cache.hip source they were taken on.
-UPD_TRAFFIC = {"source_sha256": "1c154e4c15c407c1", "workload": "wan1.3b-30layer-update", "bytes_per_call": 4259830792}
+UPD_TRAFFIC = {"source_sha256": "15da6713f8357ab0", "workload": "wan1.3b-30layer-update", "bytes_per_call": 4259822800}
 
 # HBM bytes of one spectral analysis call (all its kernels) at spectral-374clips, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE scaled by the insert copy (see profiles/spectral_fused_374clips.md); valid only for this source.

@@ -1199,9 +1199,11 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
   (void)hipGetLastError();
   const int64_t units = int64_t(c->lay.blk_bytes / 16);
   const bool bf16 = c->cfg.dtype == FADEMEM_BF16, maxop = c->cfg.merge_op == FADEMEM_MERGE_MAX;
-  // Fused updates launch the data kernel sized for kMaxPlanFrames frames;
-  // staged ones the instance sized for the plan's frames (fewer registers,
-  // more resident waves: 4% faster staged, 2% slower fused at 30 layers).
+  // Staged updates, and fused ones whose grid fits two resident rounds of
+  // the four-frame instance, launch the instance sized for the plan's frames
+  // (fewer registers, more resident waves: 6% faster staged at 30 layers, 6%
+  // faster fused at one layer); larger fused grids keep the four-frame one,
+  // which the smaller instance slowed by 2% at 30 layers.
   typedef void (*DataKernel)(UpdateDataArgs);
   static_assert(kMaxPlanFrames == 4, "one data kernel per plan size");
   static const DataKernel data_kernels[2][2][kMaxPlanFrames] = {
@@ -1245,7 +1247,10 @@ int update_impl(fademem_cache* c, const void* const* k, const void* const* v, in
       da.lay = c->lay;
       da.layer0 = l0;
       da.units = units;
-      const DataKernel data_kernel = data_kernels[bf16][maxop][staged ? nf - 1 : kMaxPlanFrames - 1];
+      const DataKernel wide = data_kernels[bf16][maxop][kMaxPlanFrames - 1];
+      const int resident = resident_blocks(reinterpret_cast<const void*>(wide), 256);
+      const bool small_grid = resident > 0 && int64_t(per_plane) * 2 * nl <= 2 * int64_t(resident);
+      const DataKernel data_kernel = (staged || small_grid) ? data_kernels[bf16][maxop][nf - 1] : wide;
       hipLaunchKernelGGL(data_kernel, dim3(per_plane, unsigned(2 * nl)), dim3(256), 0, as_stream(stream), da);
       e = hipGetLastError();
       if (e != hipSuccess) return hip_fail(c, e);
